@@ -1,0 +1,381 @@
+// The decode-step library: persistent interpreter kernel, multi-launch ablation and C ABI.
+//
+// One launch runs the whole step (arXiv 2609.12379 Sec. 4.1): each of the nwg workgroups
+// walks its own instruction queue, built on the host by fm_plan.cpp, and waits only for the
+// data its next instruction consumes. The multi-launch ablation runs the same kernel once
+// per stage, where stage = one operator of one layer.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/fm.h"
+#include "fm_device.h"
+#include "fm_ops.h"
+#include "fm_plan.h"
+
+namespace fm {
+namespace dev {
+
+template <int B, int D>
+__global__ __launch_bounds__(NT, 1) void step_kernel(Params p) {
+  __shared__ __attribute__((aligned(16))) float smem[LDS_FLOATS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wg = blockIdx.x;
+
+  // Per-lane inputs live on the device: check them here. A bad step does nothing but record
+  // the error (every workgroup reaches the same verdict).
+  u32 code = 0;
+  if (tid < p.b) {
+    const int t = p.tok[tid], ps = p.pos[tid], kl = p.kvl[tid];
+    if (t < 0 || t >= p.V) code = FM_DEV_BAD_TOKEN;
+    else if (ps < 0 || ps >= p.max_ctx) code = FM_DEV_BAD_POSITION;
+    else if (kl < 0 || kl >= p.max_ctx) code = FM_DEV_BAD_KV_LEN;
+  }
+  if (__syncthreads_or(code != 0)) {
+    if (code && wg == 0) raise_error(p, code);
+    return;
+  }
+  if (abort_raised(p)) return;
+
+  int q0, q1;
+  if (p.stage < 0) {
+    q0 = p.qoff[wg];
+    q1 = p.qoff[wg + 1];
+  } else {
+    q0 = p.stage_rng[((size_t)p.stage * p.nwg + wg) * 2];
+    q1 = p.stage_rng[((size_t)p.stage * p.nwg + wg) * 2 + 1];
+  }
+  for (int q = q0; q < q1; ++q) {
+    const int32_t* ins = p.instrs + 4 * (size_t)q;
+    const int op = ins[0];
+    bool ok = true;
+    if (op == FM_OP_ATTN) {
+      switch (p.G) {
+        case 1: ok = op_attn<D, 1>(p, ins, smem, tid, lane, wave); break;
+        case 2: ok = op_attn<D, 2>(p, ins, smem, tid, lane, wave); break;
+        case 3: case 4: ok = op_attn<D, 4>(p, ins, smem, tid, lane, wave); break;
+        default: ok = op_attn<D, 8>(p, ins, smem, tid, lane, wave); break;
+      }
+    } else if (op == FM_OP_GU) {
+      ok = op_gemv<B, 2>(p, ins, smem, tid, lane, wave);
+    } else {
+      ok = op_gemv<B, 1>(p, ins, smem, tid, lane, wave);
+    }
+    if (!ok) return;
+  }
+}
+
+}  // namespace dev
+}  // namespace fm
+
+using namespace fm;
+using namespace fm::dev;
+
+struct fm_handle {
+  fm_model_cfg cfg{};
+  int device = 0;
+  Plan plan;
+  const void* kernel = nullptr;
+  int B = 1;
+  Params base{};
+  LayerPtrs* d_layers = nullptr;
+  float* d_rope = nullptr;
+  int32_t *d_instrs = nullptr, *d_qoff = nullptr, *d_stage = nullptr;
+  u64* d_act = nullptr;
+  float* d_part = nullptr;
+  u32* d_arrive = nullptr;
+  u64* d_amax = nullptr;
+  u32* d_lm_arrive = nullptr;
+  u32* d_abort = nullptr;
+  u32* h_err = nullptr;   // pinned, device-visible
+  u32* d_err = nullptr;
+  u32 epoch = 0;
+};
+
+namespace {
+
+template <int B>
+const void* pick_kernel(int d) {
+  return d == 64 ? (const void*)&step_kernel<B, 64> : (const void*)&step_kernel<B, 128>;
+}
+
+const void* kernel_for(int Bt, int d) {
+  switch (Bt) {
+    case 1: return pick_kernel<1>(d);
+    case 2: return pick_kernel<2>(d);
+    case 4: return pick_kernel<4>(d);
+    default: return pick_kernel<8>(d);
+  }
+}
+
+int round_batch(int b) { return b <= 1 ? 1 : b <= 2 ? 2 : b <= 4 ? 4 : 8; }
+
+void free_handle(fm_handle* h) {
+  if (!h) return;
+  hipFree(h->d_layers); hipFree(h->d_rope); hipFree(h->d_instrs); hipFree(h->d_qoff);
+  hipFree(h->d_stage); hipFree(h->d_act); hipFree(h->d_part); hipFree(h->d_arrive);
+  hipFree(h->d_amax); hipFree(h->d_lm_arrive); hipFree(h->d_abort);
+  if (h->h_err) hipHostFree(h->h_err);
+  delete h;
+}
+
+struct TapOff {
+  int64_t a, qkv, qrot, krot, o, x1, a2, mlp, x2, block;
+};
+
+TapOff tap_offsets(const fm_model_cfg& c) {
+  const int64_t h = c.hidden, qd = (int64_t)c.n_heads * c.head_dim, kd = (int64_t)c.n_kv_heads * c.head_dim;
+  TapOff t;
+  t.a = 0; t.qkv = h; t.qrot = t.qkv + qd + 2 * kd; t.krot = t.qrot + qd; t.o = t.krot + kd;
+  t.x1 = t.o + qd; t.a2 = t.x1 + h; t.mlp = t.a2 + h; t.x2 = t.mlp + h; t.block = t.x2 + h;
+  return t;
+}
+
+#define HIP_TRY(x)                              \
+  do {                                          \
+    if ((x) != hipSuccess) {                    \
+      free_handle(h);                           \
+      return FM_ERR_HIP;                        \
+    }                                           \
+  } while (0)
+
+template <class T>
+hipError_t upload(T** dst, const T* src, size_t n) {
+  hipError_t e = hipMalloc((void**)dst, sizeof(T) * (n ? n : 1));
+  if (e != hipSuccess) return e;
+  return n ? hipMemcpy(*dst, src, sizeof(T) * n, hipMemcpyHostToDevice) : hipSuccess;
+}
+
+fm_status launch(fm_handle* h, const int32_t* tok, const int32_t* pos, const int32_t* kvl,
+                 float* logits, int32_t* next_ids, hipStream_t stream, bool multi) {
+  if (!h) return FM_ERR_INVALID_ARG;
+  if (!tok || !pos || !kvl || !next_ids) return FM_ERR_INVALID_ARG;
+  if (__atomic_load_n(h->h_err, __ATOMIC_ACQUIRE) != 0) return FM_ERR_DEVICE;
+  if (++h->epoch == 0) h->epoch = 1;
+  Params p = h->base;
+  p.tok = tok; p.pos = pos; p.kvl = kvl; p.logits = logits; p.next_ids = next_ids;
+  p.epoch = h->epoch;
+  if (!multi) {
+    p.stage = -1;
+    void* args[] = {&p};
+    if (hipLaunchCooperativeKernel(h->kernel, dim3(h->plan.nwg), dim3(NT), args, 0, stream) != hipSuccess)
+      return FM_ERR_HIP;
+  } else {
+    for (int s = 0; s < h->plan.n_stages; ++s) {
+      p.stage = s;
+      void* args[] = {&p};
+      if (hipLaunchKernel(h->kernel, dim3(h->plan.nwg), dim3(NT), args, 0, stream) != hipSuccess)
+        return FM_ERR_HIP;
+    }
+  }
+  return FM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* fm_status_string(fm_status s) {
+  switch (s) {
+    case FM_OK: return "ok";
+    case FM_ERR_INVALID_ARG: return "invalid argument";
+    case FM_ERR_UNSUPPORTED: return "unsupported shape";
+    case FM_ERR_CAPACITY: return "capacity exceeded";
+    case FM_ERR_HIP: return "HIP runtime error";
+    case FM_ERR_DEVICE: return "device-side error recorded";
+  }
+  return "unknown status";
+}
+
+size_t fm_tap_count(const fm_model_cfg* cfg) {
+  if (!cfg) return 0;
+  TapOff t = tap_offsets(*cfg);
+  return (size_t)cfg->n_layers * cfg->batch * t.block + (size_t)cfg->batch * cfg->hidden;
+}
+
+fm_status fm_plan_query(const fm_model_cfg* cfg, int32_t n_cu, fm_plan_stats* out) {
+  if (!cfg || !out) return FM_ERR_INVALID_ARG;
+  Plan p;
+  fm_status st = build_plan(*cfg, n_cu, p, nullptr);
+  if (st != FM_OK) return st;
+  *out = p.stats;
+  return FM_OK;
+}
+
+fm_status fm_plan_export(const fm_model_cfg* cfg, int32_t n_cu, int32_t* qoff, int32_t qoff_cap,
+                         int32_t* instrs, int32_t instr_cap) {
+  if (!cfg || !qoff || !instrs) return FM_ERR_INVALID_ARG;
+  Plan p;
+  fm_status st = build_plan(*cfg, n_cu, p, nullptr);
+  if (st != FM_OK) return st;
+  if (qoff_cap < (int32_t)p.qoff.size() || instr_cap < (int32_t)p.instrs.size() * 4) return FM_ERR_CAPACITY;
+  std::memcpy(qoff, p.qoff.data(), sizeof(int32_t) * p.qoff.size());
+  std::memcpy(instrs, p.instrs.data(), sizeof(Instr) * p.instrs.size());
+  return FM_OK;
+}
+
+fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_kv_ptrs* kv, fm_handle** out) {
+  if (out) *out = nullptr;
+  if (!cfg || !w || !kv || !out || !w->layers || !kv->k || !kv->v || !w->embed || !w->final_norm)
+    return FM_ERR_INVALID_ARG;
+  const fm_model_cfg& c = *cfg;
+  if (!c.tied_embedding && !w->lm_head) return FM_ERR_INVALID_ARG;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const fm_layer_weights& L = w->layers[l];
+    if (!L.attn_norm || !L.w_q || !L.w_k || !L.w_v || !L.w_o || !L.mlp_norm || !L.w_gate || !L.w_up ||
+        !L.w_down || !kv->k[l] || !kv->v[l])
+      return FM_ERR_INVALID_ARG;
+    if (c.qk_norm && (!L.q_norm || !L.k_norm)) return FM_ERR_INVALID_ARG;
+  }
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return FM_ERR_HIP;
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return FM_ERR_HIP;
+  const int nwg = c.n_workgroups > 0 ? c.n_workgroups : prop.multiProcessorCount;
+
+  fm_handle* h = new fm_handle();
+  h->cfg = c;
+  h->device = dev;
+  fm_status st = build_plan(c, nwg, h->plan, nullptr);
+  if (st != FM_OK) { free_handle(h); return st; }
+  const Plan& P = h->plan;
+
+  // Capacity: 32-bit buffer offsets (matrices, KV arenas, scratch), LDS tiles.
+  const int64_t L = c.n_layers, hd = c.hidden, d = c.head_dim, nh = c.n_heads, nkv = c.n_kv_heads;
+  const int64_t inter = c.intermediate, V = c.vocab, b = c.batch;
+  const int64_t nqkv = (nh + 2 * nkv) * d;
+  const int64_t biggest = std::max({V * hd, nqkv * hd, inter * hd, hd * nh * d}) * 2;
+  const int64_t arena = b * nkv * (int64_t)c.max_ctx * d * 2;
+  const int64_t words = (L + 1) * b * hd + L * b * (nqkv + nh * d + hd + inter);
+  h->B = round_batch(c.batch);
+  const int Bt = h->B;
+  if (biggest >= (1ll << 31) || arena >= (1ll << 31) || words * 8 >= (1ll << 32)) { free_handle(h); return FM_ERR_CAPACITY; }
+  {
+    // Per-tile LDS needs: residual rows, and per-row partials when K spans several slabs.
+    auto rows_max = [&](int64_t n) { return (n + nwg - 1) / nwg; };
+    if (rows_max(hd) * Bt > RESID_FLOATS) { free_handle(h); return FM_ERR_CAPACITY; }
+    const int64_t ks = (XSLAB_FLOATS / Bt) & ~511;
+    auto needs = [&](int64_t K, int64_t rows, int nw) { return K > ks ? rows_max(rows) * nw * Bt : 0; };
+    if (needs(hd, nqkv, 1) > ROWACC_FLOATS || needs(nh * d, hd, 1) > ROWACC_FLOATS ||
+        needs(hd, inter, 2) > ROWACC_FLOATS || needs(inter, hd, 1) > ROWACC_FLOATS ||
+        needs(hd, V, 1) > ROWACC_FLOATS) {
+      free_handle(h);
+      return FM_ERR_CAPACITY;
+    }
+  }
+  h->kernel = kernel_for(Bt, (int)d);
+  int occ = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, h->kernel, NT, 0) != hipSuccess) { free_handle(h); return FM_ERR_HIP; }
+  if ((int64_t)occ * prop.multiProcessorCount < nwg) { free_handle(h); return FM_ERR_CAPACITY; }
+
+  // Weight pointer table.
+  std::vector<LayerPtrs> lp(L);
+  for (int l = 0; l < L; ++l) {
+    const fm_layer_weights& s = w->layers[l];
+    lp[l] = LayerPtrs{(const uint16_t*)s.attn_norm, (const uint16_t*)s.w_q, (const uint16_t*)s.w_k,
+                      (const uint16_t*)s.w_v, (const uint16_t*)s.q_norm, (const uint16_t*)s.k_norm,
+                      (const uint16_t*)s.w_o, (const uint16_t*)s.mlp_norm, (const uint16_t*)s.w_gate,
+                      (const uint16_t*)s.w_up, (const uint16_t*)s.w_down, (uint16_t*)kv->k[l],
+                      (uint16_t*)kv->v[l]};
+  }
+  HIP_TRY(upload(&h->d_layers, lp.data(), lp.size()));
+  // Rotary table: angle pos * theta^(-2e/d) in double, cos/sin rounded to fp32.
+  {
+    const int half = (int)d / 2;
+    std::vector<float> rt((size_t)c.max_ctx * half * 2);
+    for (int ps = 0; ps < c.max_ctx; ++ps)
+      for (int e = 0; e < half; ++e) {
+        const double ang = (double)ps * std::pow(c.rope_theta, -2.0 * (double)e / (double)d);
+        rt[((size_t)ps * half + e) * 2] = (float)std::cos(ang);
+        rt[((size_t)ps * half + e) * 2 + 1] = (float)std::sin(ang);
+      }
+    HIP_TRY(upload(&h->d_rope, rt.data(), rt.size()));
+  }
+  HIP_TRY(upload(&h->d_instrs, (const int32_t*)P.instrs.data(), P.instrs.size() * 4));
+  HIP_TRY(upload(&h->d_qoff, P.qoff.data(), P.qoff.size()));
+  HIP_TRY(upload(&h->d_stage, P.stage_rng.data(), P.stage_rng.size()));
+  HIP_TRY(hipMalloc(&h->d_act, words * 8));
+  HIP_TRY(hipMemset(h->d_act, 0, words * 8));
+  const size_t part_floats = (size_t)b * nh * P.attn_max_chunks * (d + 2);
+  HIP_TRY(hipMalloc(&h->d_part, part_floats * 4));
+  HIP_TRY(hipMemset(h->d_part, 0, part_floats * 4));
+  HIP_TRY(hipMalloc(&h->d_arrive, b * nkv * 4));
+  HIP_TRY(hipMemset(h->d_arrive, 0, b * nkv * 4));
+  HIP_TRY(hipMalloc(&h->d_amax, b * 8));
+  HIP_TRY(hipMemset(h->d_amax, 0, b * 8));
+  HIP_TRY(hipMalloc(&h->d_lm_arrive, 64));
+  HIP_TRY(hipMemset(h->d_lm_arrive, 0, 64));
+  HIP_TRY(hipMalloc(&h->d_abort, 64));
+  HIP_TRY(hipMemset(h->d_abort, 0, 64));
+  HIP_TRY(hipHostMalloc((void**)&h->h_err, 64, hipHostMallocMapped));
+  std::memset(h->h_err, 0, 64);
+  HIP_TRY(hipHostGetDevicePointer((void**)&h->d_err, h->h_err, 0));
+
+  Params& p = h->base;
+  p.L = (int32_t)L; p.h = (int32_t)hd; p.nh = (int32_t)nh; p.nkv = (int32_t)nkv; p.d = (int32_t)d;
+  p.inter = (int32_t)inter; p.V = (int32_t)V; p.b = (int32_t)b; p.max_ctx = c.max_ctx;
+  p.qk_norm = c.qk_norm; p.G = (int32_t)(nh / nkv);
+  p.nwg = nwg; p.P = P.attn_items; p.maxc = P.attn_max_chunks; p.n_lm_instr = P.n_lm_instr;
+  p.eps = (float)c.rms_eps;
+  p.q_scale = (float)(1.4426950408889634 / std::sqrt((double)d));
+  p.layers = h->d_layers;
+  p.embed = (const uint16_t*)w->embed;
+  p.final_norm = (const uint16_t*)w->final_norm;
+  p.lm_head = (const uint16_t*)(c.tied_embedding ? w->embed : w->lm_head);
+  p.rope = h->d_rope;
+  p.instrs = h->d_instrs; p.qoff = h->d_qoff; p.stage_rng = h->d_stage; p.stage = -1;
+  p.act = h->d_act; p.act_bytes = (u32)(words * 8);
+  p.st_x = (u32)(b * hd); p.st_qkv = (u32)(b * nqkv); p.st_o = (u32)(b * nh * d);
+  p.st_x1 = (u32)(b * hd); p.st_m = (u32)(b * inter);
+  p.off_x = 0;
+  p.off_qkv = p.off_x + (u32)(L + 1) * p.st_x;
+  p.off_o = p.off_qkv + (u32)L * p.st_qkv;
+  p.off_x1 = p.off_o + (u32)L * p.st_o;
+  p.off_m = p.off_x1 + (u32)L * p.st_x1;
+  p.part = h->d_part; p.arrive = h->d_arrive; p.amax = h->d_amax; p.lm_arrive = h->d_lm_arrive;
+  p.abort_flag = h->d_abort; p.err_host = h->d_err;
+  const TapOff t = tap_offsets(c);
+  p.taps = nullptr; p.tap_block = t.block;
+  p.tap_a = (int32_t)t.a; p.tap_qkv = (int32_t)t.qkv; p.tap_qrot = (int32_t)t.qrot; p.tap_krot = (int32_t)t.krot;
+  p.tap_o = (int32_t)t.o; p.tap_x1 = (int32_t)t.x1; p.tap_a2 = (int32_t)t.a2; p.tap_mlp = (int32_t)t.mlp;
+  p.tap_x2 = (int32_t)t.x2;
+  *out = h;
+  return FM_OK;
+}
+
+fm_status fm_decode_step(fm_handle* h, const int32_t* token_ids, const int32_t* positions,
+                         const int32_t* kv_lens, float* logits_out, int32_t* next_ids, hipStream_t stream) {
+  return launch(h, token_ids, positions, kv_lens, logits_out, next_ids, stream, false);
+}
+
+fm_status fm_decode_step_multilaunch(fm_handle* h, const int32_t* token_ids, const int32_t* positions,
+                                     const int32_t* kv_lens, float* logits_out, int32_t* next_ids,
+                                     hipStream_t stream) {
+  return launch(h, token_ids, positions, kv_lens, logits_out, next_ids, stream, true);
+}
+
+fm_status fm_destroy(fm_handle* h) {
+  if (!h) return FM_ERR_INVALID_ARG;
+  hipDeviceSynchronize();
+  free_handle(h);
+  return FM_OK;
+}
+
+fm_status fm_last_error(fm_handle* h, int32_t* device_code) {
+  if (!h || !device_code) return FM_ERR_INVALID_ARG;
+  if (hipDeviceSynchronize() != hipSuccess) return FM_ERR_HIP;
+  *device_code = (int32_t)__atomic_load_n(h->h_err, __ATOMIC_ACQUIRE);
+  return *device_code ? FM_ERR_DEVICE : FM_OK;
+}
+
+fm_status fm_set_taps(fm_handle* h, float* tap_buf) {
+  if (!h) return FM_ERR_INVALID_ARG;
+  h->base.taps = tap_buf;
+  return FM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,141 @@
+// Host-side schedule compiler (see fm_plan.h).
+#include "fm_plan.h"
+
+#include <algorithm>
+#include <cstdio>
+
+namespace fm {
+
+namespace {
+
+bool fail(std::string* why, const char* msg) {
+  if (why) *why = msg;
+  return false;
+}
+
+bool check_cfg(const fm_model_cfg& c, std::string* why, fm_status* st) {
+  *st = FM_ERR_INVALID_ARG;
+  if (c.n_layers < 1 || c.hidden < 1 || c.n_heads < 1 || c.n_kv_heads < 1 || c.head_dim < 1 ||
+      c.intermediate < 1 || c.vocab < 1 || c.batch < 1 || c.max_ctx < 1 || c.n_workgroups < 0 ||
+      c.attn_items < 0 || c.reserved != 0)
+    return fail(why, "dimensions must be positive (n_workgroups, attn_items >= 0, reserved == 0)");
+  if (c.n_heads % c.n_kv_heads != 0) return fail(why, "n_heads must be a multiple of n_kv_heads");
+  if (!(c.rope_theta > 0.0) || !(c.rms_eps >= 0.0)) return fail(why, "rope_theta > 0 and rms_eps >= 0 required");
+  *st = FM_ERR_UNSUPPORTED;
+  if (c.head_dim != 64 && c.head_dim != 128) return fail(why, "head_dim must be 64 or 128");
+  if (c.n_heads / c.n_kv_heads > 8) return fail(why, "n_heads / n_kv_heads must be <= 8");
+  if (c.batch > 8) return fail(why, "batch must be <= 8");
+  if (c.hidden % 8 || (c.n_heads * c.head_dim) % 8 || c.intermediate % 8)
+    return fail(why, "hidden, n_heads*head_dim and intermediate must be multiples of 8");
+  return true;
+}
+
+// Balanced contiguous split of [0, n) into nwg parts; part w is [lo, hi).
+void split(int64_t n, int32_t nwg, int32_t w, int32_t& lo, int32_t& hi) {
+  lo = (int32_t)(n * w / nwg);
+  hi = (int32_t)(n * (w + 1) / nwg);
+}
+
+}  // namespace
+
+fm_status build_plan(const fm_model_cfg& c, int32_t nwg, Plan& p, std::string* why) {
+  fm_status st;
+  if (!check_cfg(c, why, &st)) return st;
+  if (nwg < 1) {
+    if (why) *why = "need at least one workgroup";
+    return FM_ERR_INVALID_ARG;
+  }
+  const int32_t L = c.n_layers, h = c.hidden, d = c.head_dim, nh = c.n_heads, nkv = c.n_kv_heads;
+  const int32_t inter = c.intermediate, V = c.vocab, b = c.batch;
+  const int64_t qkv_rows = (int64_t)(nh + 2 * nkv) * d;
+
+  // Attention work items per layer. Each (lane, KV head) needs at least one item, and the
+  // per-step chunking (see the kernel's item map) needs P > n_kv * b.
+  int32_t P = c.attn_items;
+  if (P == 0) {
+    int32_t need = nkv * b;
+    P = nwg;
+    if (need > nwg / 2) P = nwg * ((need + nwg + nwg - 1) / nwg);
+  }
+  if (P <= nkv * b) {
+    if (why) *why = "attn_items must exceed n_kv_heads * batch";
+    return FM_ERR_INVALID_ARG;
+  }
+  p = Plan();
+  p.nwg = nwg;
+  p.attn_items = P;
+  p.attn_max_chunks = (P - nkv * b) / nkv + 1;
+  p.n_stages = 5 * L + 1;
+
+  std::vector<std::vector<Instr>> q(nwg);
+  std::vector<double> bytes(nwg, 0.0);
+  auto gemv = [&](int32_t op, int32_t l, int64_t rows, int64_t K, int32_t nw) {
+    for (int32_t w = 0; w < nwg; ++w) {
+      int32_t lo, hi;
+      split(rows, nwg, w, lo, hi);
+      if (hi > lo) {
+        q[w].push_back(Instr{op, l, lo, hi});
+        bytes[w] += (double)(hi - lo) * K * 2.0 * nw;
+      }
+    }
+  };
+  for (int32_t l = 0; l < L; ++l) {
+    gemv(FM_OP_QKV, l, qkv_rows, h, 1);
+    for (int32_t j = 0; j < P; ++j) q[j % nwg].push_back(Instr{FM_OP_ATTN, l, j, 0});
+    gemv(FM_OP_OPROJ, l, h, (int64_t)nh * d, 1);
+    gemv(FM_OP_GU, l, inter, h, 2);
+    gemv(FM_OP_DOWN, l, h, inter, 1);
+  }
+  gemv(FM_OP_LM, L, V, h, 1);
+
+  p.qoff.assign(nwg + 1, 0);
+  p.stage_rng.assign((size_t)p.n_stages * nwg * 2, 0);
+  int32_t lm = 0;
+  for (int32_t w = 0; w < nwg; ++w) {
+    p.qoff[w] = (int32_t)p.instrs.size();
+    int32_t base = (int32_t)p.instrs.size();
+    for (size_t k = 0; k < q[w].size(); ++k) {
+      const Instr& in = q[w][k];
+      int32_t s = stage_of(in, L);
+      int32_t* r = &p.stage_rng[((size_t)s * nwg + w) * 2];
+      int32_t idx = base + (int32_t)k;
+      if (r[1] == r[0]) r[0] = idx;
+      r[1] = idx + 1;
+      if (in.op == FM_OP_LM) ++lm;
+      p.instrs.push_back(in);
+    }
+  }
+  p.qoff[nwg] = (int32_t)p.instrs.size();
+  p.n_lm_instr = lm;
+
+  // Statistics (the paper's interpreter gate: instruction types, instructions per layer,
+  // queue imbalance; its dependency gate: distinct counters).
+  fm_plan_stats& s = p.stats;
+  s.n_cu = nwg;
+  s.n_instr = (int32_t)p.instrs.size();
+  s.n_types = 6;
+  int32_t min_pl = 1 << 30;
+  for (int32_t l = 0; l < L; ++l) {
+    int32_t cnt = 0;
+    for (const Instr& in : p.instrs) cnt += (in.layer == l && in.op != FM_OP_LM);
+    min_pl = std::min(min_pl, cnt);
+  }
+  s.min_instr_per_layer = min_pl;
+  // Per layer: tagged qkv, o, x1, m and x vectors (5) plus one arrival counter per
+  // (lane, KV head); per step: the LM arrival counter and b argmax words.
+  s.n_counters = 5 * L + nkv * b + 1 + b;
+  s.attn_items = P;
+  s.attn_max_chunks = p.attn_max_chunks;
+  s.n_stages = p.n_stages;
+  double mx = 0, sum = 0;
+  for (double v : bytes) {
+    mx = std::max(mx, v);
+    sum += v;
+  }
+  s.max_bytes_per_cu = mx;
+  s.mean_bytes_per_cu = sum / nwg;
+  s.imbalance = sum > 0 ? mx / (sum / nwg) : 1.0;
+  return FM_OK;
+}
+
+}  // namespace fm

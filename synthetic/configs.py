@@ -45,6 +45,8 @@ CONFIGS = {
     # small shapes for CPU-time parity
     "toy": _c(k=10, n_layers=2, hidden=64, n_heads=4, n_kv_heads=2, head_dim=16, intermediate=96,
               vocab=200, qk_norm=1, rope_theta=1e4, rms_eps=1e-6, batch=2, ctx=(5, 12), steps=4),
+    "toy-gpu": _c(k=16, n_layers=2, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64, intermediate=392,
+                  vocab=1000, qk_norm=1, rope_theta=1e4, rms_eps=1e-6, batch=2, ctx=(5, 40), steps=4),
     "mini-qwen3": _c(k=11, n_layers=3, hidden=1024, n_heads=16, n_kv_heads=8, head_dim=128,
                      intermediate=1376, vocab=5003, qk_norm=1, tied_embedding=1, rope_theta=1e6,
                      rms_eps=1e-6, batch=1, ctx=(300, 300), steps=3),
@@ -52,7 +54,7 @@ CONFIGS = {
                       intermediate=2200, vocab=7001, tied_embedding=1, rope_theta=5e5,
                       batch=1, ctx=(700, 700), steps=3),
     "mini-llama2": _c(k=13, n_layers=2, hidden=1536, n_heads=12, n_kv_heads=12, head_dim=128,
-                      intermediate=4100, vocab=3000, batch=1, ctx=(129, 129), steps=3),
+                      intermediate=4104, vocab=3000, batch=1, ctx=(129, 129), steps=3),
     "mini-qwen3-b4": _c(k=14, n_layers=2, hidden=1024, n_heads=8, n_kv_heads=2, head_dim=128,
                         intermediate=2816, vocab=4099, qk_norm=1, rope_theta=1e6, rms_eps=1e-6,
                         batch=4, ctx=(1, 900), steps=3),

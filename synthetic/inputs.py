@@ -95,8 +95,12 @@ def make_kv(cfg: dict, S: list, max_ctx: int, seed: int | None = None, poison: b
         t = torch.zeros((b, nkv, max_ctx, d), dtype=torch.bfloat16)
         for i in range(b):
             t[i, :, : S[i], :] = torch.randn((nkv, S[i], d), generator=g).to(torch.bfloat16)
-            if poison and S[i] < max_ctx:
-                t[i, :, S[i]:, :] = (torch.randn((nkv, max_ctx - S[i], d), generator=g) * 100.0).to(torch.bfloat16)
+        if poison:
+            # a separate stream, so the prefill is identical with and without poison
+            gp = torch.Generator().manual_seed((seed * 1_000_003 + idx * 104729 + 1) % (2**62))
+            for i in range(b):
+                if S[i] < max_ctx:
+                    t[i, :, S[i]:, :] = (torch.randn((nkv, max_ctx - S[i], d), generator=gp) * 100.0).to(torch.bfloat16)
         return t
 
     with ThreadPoolExecutor(max_workers=threads) as ex:
