@@ -1,0 +1,209 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark: one persistent-kernel decode step on one MI355X.
+
+Default workload: a Llama-3.2-1B-shaped decoder (16 layers, hidden 2048, 32/8 heads of 64,
+SwiGLU 8192, vocab 128256, tied embedding), random bf16 weights N(0, 0.02), batch 1,
+KV prefilled to context 2048, greedy decode. A "step" generates one token per lane: embedding,
+all layers, final norm, LM head and argmax, in one kernel launch. Step t feeds its greedy
+token to step t+1 on the device; positions and cache lengths (S + t) are uploaded before the
+timed region.
+
+Printed as one JSON line (rank 0): latency per step (us/token), Eq. 2 bytes and MBU against
+the 8 TB/s HBM3E peak, a roofline object for the kernel, the multi-launch ablation (one
+launch per operator stage) on the same inputs, and the CPU reference decoder timed on a
+bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode step latency (µs/token) and MBU % of MI355X HBM peak, batch 1"
+PEAK_GBS = 8000.0
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--config", default="llama3.2-1b")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU reference leg")
+    ap.add_argument("--no-ablation", action="store_true", help="skip the multi-launch ablation")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU sample")
+    ap.add_argument("--calib-copy-mb", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--nwg", type=int, default=0)
+    ap.add_argument("--attn-items", type=int, default=0)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from synthetic import get_config, make_workload, as_u16
+    from paper_2609_12379_amd.fm import Decoder, load
+    from paper_2609_12379_amd.metrics import step_bytes
+
+    load()  # fail loudly if the HIP library is missing
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    cfg0 = get_config(args.config)
+    total_steps = args.warmup + args.steps
+    t_gen = time.time()
+    wl = make_workload(cfg0, steps=max(total_steps, cfg0["steps"]), threads=16)
+    cfg = wl.cfg
+    gen_s = time.time() - t_gen
+    b = cfg["batch"]
+
+    wdev = {k: v.cuda() for k, v in wl.weights.items() if k != "layers" and v is not None}
+    wdev["layers"] = [{k: v.cuda() for k, v in lw.items()} for lw in wl.weights["layers"]]
+    kc = [t.cuda() for t in wl.kcache]
+    vc = [t.cuda() for t in wl.vcache]
+    dec = Decoder(cfg, wdev, kc, vc, n_workgroups=args.nwg, attn_items=args.attn_items)
+
+    S = wl.S
+    pos_all = torch.tensor([[s + t for s in S] for t in range(total_steps)], dtype=torch.int32, device="cuda")
+    logits = torch.empty((b, cfg["vocab"]), dtype=torch.float32, device="cuda")
+    ids = torch.empty((total_steps + 1, b), dtype=torch.int32, device="cuda")
+    ids[0] = torch.tensor(wl.start, dtype=torch.int32)
+
+    def run(t, multilaunch=False):
+        dec.step(ids[t], pos_all[t], pos_all[t], logits, ids[t + 1], multilaunch=multilaunch)
+
+    for t in range(args.warmup):
+        run(t)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    e0.record(stream)
+    for t in range(args.warmup, total_steps):
+        run(t)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - w0) * 1e3
+    ev_ms = e0.elapsed_time(e1)
+    ms_per_step = ev_ms / args.steps
+    assert dec.last_error() == 0, "device reported an error"
+    assert bool(torch.isfinite(logits).all()), "non-finite logits"
+
+    # Eq. 2 bytes of each timed step: attention reads kv_len + 1 slots per lane.
+    bytes_steps = [step_bytes(cfg, [s + t + 1 for s in S]) for t in range(args.warmup, total_steps)]
+    mean_bytes = sum(bytes_steps) / len(bytes_steps)
+    achieved_gbs = mean_bytes / (ms_per_step * 1e-3) / 1e9
+    mbu = sum(bytes_steps) / (ev_ms * 1e-3) / (PEAK_GBS * 1e9)
+
+    # Two-point slope (the paper's latency estimate): min over replicates of
+    # (t(N2) - t(N1)) / (N2 - N1), steps replayed from the warm state.
+    def timed(n, multilaunch=False):
+        torch.cuda.synchronize()
+        a, c = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for t in range(n):
+            run(args.warmup + t, multilaunch)
+        c.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(c)
+
+    n2 = args.steps
+    n1 = max(1, n2 // 4)
+    slopes = []
+    for _ in range(3):
+        slopes.append((timed(n2) - timed(n1)) / (n2 - n1))
+    slope_ms = min(slopes)
+
+    out = {
+        "metric": METRIC,
+        "value": round(ms_per_step * 1e3, 2),
+        "unit": "us/token",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "storage": "bf16 weights and KV cache",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg['name']}-shaped decoder, b{b}, context {S if len(set(S)) > 1 else S[0]}, "
+                               f"greedy decode",
+                   "layers": cfg["n_layers"], "hidden": cfg["hidden"], "heads": [cfg["n_heads"], cfg["n_kv_heads"]],
+                   "head_dim": cfg["head_dim"], "intermediate": cfg["intermediate"], "vocab": cfg["vocab"],
+                   "batch": b, "context": S, "timing_scope": "step with greedy argmax, inputs resident in HBM"},
+        "mbu_pct": round(100 * mbu, 2),
+        "bytes_per_step_eq2": int(mean_bytes),
+        "two_point_slope_us": round(slope_ms * 1e3, 2),
+        "wall_ms_timed_region": round(wall_ms, 3),
+        "roofline": {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved_gbs / PEAK_GBS, 4), "traffic": None,
+                     "kernel": "fm::dev::step_kernel (one launch per step)"},
+    }
+
+    if not args.no_ablation:
+        # Multi-launch ablation: the same device code launched once per operator stage.
+        for t in range(2):
+            run(args.warmup + t, True)
+        torch.cuda.synchronize()
+        ml = timed(args.steps, True) / args.steps
+        out["ablation_multilaunch"] = {"ms_per_step": round(ml, 5), "us_per_token": round(ml * 1e3, 2),
+                                       "mbu_pct": round(100 * sum(bytes_steps) / (ml * args.steps * 1e-3) / (PEAK_GBS * 1e9), 2),
+                                       "launches_per_step": 5 * cfg["n_layers"] + 1,
+                                       "megakernel_speedup": round(ml / ms_per_step, 3)}
+
+    if args.calib_copy_mb:
+        n = args.calib_copy_mb * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["calib_copy_bytes_each_way"] = n * 4
+
+    if not args.no_cpu:
+        # CPU reference decoder on this host: a bounded sample of the same workload.
+        from oracle.oracle import Oracle
+        wu = {k: as_u16(v) for k, v in wl.weights.items() if k != "layers" and v is not None}
+        wu["layers"] = [{k: as_u16(v) for k, v in lw.items()} for lw in wl.weights["layers"]]
+        orc = Oracle(cfg, wu)
+        kco = [as_u16(t).copy() for t in wl.kcache]
+        vco = [as_u16(t).copy() for t in wl.vcache]
+        threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+        tok = list(wl.start)
+        n_cpu, t_cpu = 0, 0.0
+        while n_cpu < 2 or (t_cpu < args.cpu_seconds and n_cpu < args.steps):
+            pos = [s + n_cpu for s in S]
+            c0 = time.perf_counter()
+            r = orc.step(kco, vco, tok, pos, pos, precision="f32")
+            t_cpu += time.perf_counter() - c0
+            tok = [int(v) for v in r.next_ids]
+            n_cpu += 1
+        model = ""
+        try:
+            with open("/proc/cpuinfo") as f:
+                for line in f:
+                    if line.startswith("model name"):
+                        model = line.split(":", 1)[1].strip()
+                        break
+        except OSError:
+            pass
+        out["cpu_baseline"] = {"value": round(t_cpu / n_cpu * 1e6, 1), "unit": "us/token", "cores": threads,
+                               "kind": "oracle", "cpu_model": model,
+                               "sample": f"first {n_cpu} greedy steps of the same workload (fp32 oracle, "
+                                         f"{t_cpu:.1f} s of CPU time)"}
+    out["setup_s"] = round(gen_s, 1)
+    print(json.dumps(out), flush=True)
+    dec.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -8,12 +8,14 @@
 //     counter, so a handoff costs one store and one read round trip. There is no separate
 //     flag, no grid barrier, and no L2 writeback or invalidate (both cost microseconds on
 //     MI355X's eight non-coherent XCD L2s).
-//   * Attention partials use plain fp32 sc1 stores, published by an arrival counter that
-//     is incremented after the stores complete.
+//   * Attention partials are tagged words too; each (lane, KV head) has a combine
+//     instruction that waits for all of its chunks' partials.
 //   * Weights and the KV cache are streamed with non-temporal 128-bit buffer loads.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include "fm_limits.h"
 
 namespace fm {
 namespace dev {
@@ -24,10 +26,21 @@ typedef u32 u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int NT = 512;              // threads per workgroup
 constexpr int NWAVE = NT / 64;
-constexpr int XSLAB_FLOATS = 24576;  // activation slab (96 KB)
-constexpr int ROWACC_FLOATS = 4096;  // per-row partial sums across slabs (16 KB)
+// Wave roles inside a GEMV tile: streaming waves only load weights; control waves only poll
+// and stage the inputs. A wave's memory operations complete in issue order, so a wave that
+// polled its input behind its own weight prefetch would see the input only after the
+// prefetch landed.
+// Measured on MI355X: splitting roles (2 control + 6 streaming waves) was slower than
+// letting all 8 waves do both, so NCTL = 0 (every wave streams and stages).
+#ifndef FM_RING
+#define FM_RING 16
+#endif
+constexpr int NCTL = 0;
+constexpr int NSW = NWAVE - NCTL;
+constexpr int XSLAB_FLOATS = kSlabFloats;  // activation slab / combine staging (96 KB)
+constexpr int ROWACC_FLOATS = 8192;  // per-row dot products (and partials across slabs), 32 KB
 constexpr int RESID_FLOATS = 2048;   // residual rows staged for the epilogue (8 KB)
-constexpr int MISC_FLOATS = 512;
+constexpr int MISC_FLOATS = 1024;
 constexpr int LDS_FLOATS = XSLAB_FLOATS + ROWACC_FLOATS + RESID_FLOATS + MISC_FLOATS;
 
 constexpr u32 CPOL_NT = 2;    // non-temporal (streaming)
@@ -38,7 +51,7 @@ struct LayerPtrs {
   uint16_t *kc, *vc;
 };
 
-// Everything one launch needs; passed by value.
+// Everything about the model and the handle's scratch; uploaded once to device memory.
 struct Params {
   // shape
   int32_t L, h, nh, nkv, d, inter, V, b, max_ctx, qk_norm, G;
@@ -52,29 +65,46 @@ struct Params {
   const int32_t* instrs;         // [n][4]
   const int32_t* qoff;           // [nwg + 1]
   const int32_t* stage_rng;      // [n_stages][nwg][2]
-  int32_t stage;                 // -1: whole step in one launch; else one stage
   // scratch: tagged words, word offsets into `act`
   u64* act;
   u32 act_bytes;
   u32 off_x, off_qkv, off_o, off_x1, off_m;      // bases; per-layer strides below
   u32 st_x, st_qkv, st_o, st_x1, st_m;           // words per layer (all lanes)
-  float* part;                   // [b][nh][maxc][d + 2]
-  u32* arrive;                   // [b][nkv]
+  const uint16_t* zero_page;      // 64 KiB of zeros: the target of loads with nothing to load
+  u64* part;                     // tagged [L][b][nh][maxc][d + 2]: split-KV partials
   u64* amax;                     // [b]
   u32* lm_arrive;                // [1]
   u32* abort_flag;               // [1]
   u32* err_host;                 // pinned host word
-  // per step
+  int64_t tap_block;             // floats per (layer, lane) block
+  int32_t tap_a, tap_qkv, tap_qrot, tap_krot, tap_o, tap_x1, tap_a2, tap_mlp, tap_x2;
+};
+
+// Params is read through the constant address space: scalar loads that no store can alias,
+// so reading a field never stalls on (or is re-issued after) outstanding memory operations.
+typedef __attribute__((address_space(4))) const Params CParams;
+typedef __attribute__((address_space(4))) const LayerPtrs CLayerPtrs;
+
+// Per-step arguments, passed by value with each launch (Params lives in device memory).
+struct Step {
   const int32_t *tok, *pos, *kvl;
   float* logits;
   int32_t* next_ids;
-  float* taps;
-  int64_t tap_block;             // floats per (layer, lane) block
-  int32_t tap_a, tap_qkv, tap_qrot, tap_krot, tap_o, tap_x1, tap_a2, tap_mlp, tap_x2;
+  float* taps;                   // optional mid-state taps
+  u64* timeline;                 // optional: per instruction {start, inputs ready, end, wg}
   u32 epoch;
+  int32_t stage;                 // -1: whole step in one launch; else one stage
 };
 
 // ---- small helpers ---------------------------------------------------------------------
+
+typedef __attribute__((address_space(1))) const u32x4 global_u32x4;
+
+// 16-byte non-temporal load through the global (not flat) address space, so it is tracked
+// by vmcnt only and never delays an LDS wait.
+__device__ __forceinline__ u32x4 ld_stream16(const void* p) {
+  return __builtin_nontemporal_load((const global_u32x4*)p);
+}
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, u32 bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
@@ -113,6 +143,50 @@ __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
+}
+
+// Sum within each 16-lane row; every lane of the row gets the total (DPP, no LDS).
+__device__ __forceinline__ float row16_sum(float s) {
+  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0xB1, 0xF, 0xF, false));   // quad [1,0,3,2]
+  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x4E, 0xF, 0xF, false));   // quad [2,3,0,1]
+  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x141, 0xF, 0xF, false));  // half-row mirror
+  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x140, 0xF, 0xF, false));  // row mirror
+  return s;
+}
+
+// Transpose-reduce of four per-lane partial sums a0..a3 over the 64 lanes of a wave.
+// Returns, in every lane of 16-lane row R, the full sum of a_{map(R)} with
+// map = {0, 2, 1, 3}: lanes 0-15 hold sum(a0), 16-31 sum(a2), 32-47 sum(a1), 48-63 sum(a3).
+// gfx950's v_permlane32_swap / v_permlane16_swap exchange half-waves / half-rows in the VALU.
+__device__ __forceinline__ float reduce4(float a0, float a1, float a2, float a3) {
+  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(a0), __float_as_uint(a1), false, false);
+  const float s01 = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(a2), __float_as_uint(a3), false, false);
+  const float s23 = __uint_as_float(q[0]) + __uint_as_float(q[1]);
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(s01), __float_as_uint(s23), false, false);
+  return row16_sum(__uint_as_float(r[0]) + __uint_as_float(r[1]));
+}
+
+// Same for two rows: lanes 0-31 hold sum(a0), lanes 32-63 sum(a1).
+__device__ __forceinline__ float reduce2(float a0, float a1) {
+  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(a0), __float_as_uint(a1), false, false);
+  const float s = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(s), __float_as_uint(s), false, false);
+  return row16_sum(__uint_as_float(r[0]) + __uint_as_float(r[1]));
+}
+
+// Full 64-lane sum in every lane.
+__device__ __forceinline__ float reduce1(float a) {
+  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(a), false, false);
+  const float s = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(s), __float_as_uint(s), false, false);
+  return row16_sum(__uint_as_float(r[0]) + __uint_as_float(r[1]));
+}
+
+// Value of lane (l xor 32).
+__device__ __forceinline__ float swap_halves(float v) {
+  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(p[1]);
 }
 
 __device__ __forceinline__ u64 clock_now() { return wall_clock64(); }

@@ -1,0 +1,81 @@
+// The step interpreter kernel (one persistent launch per step, or one launch per stage).
+// Each workgroup walks its own instruction queue, built on the host by fm_plan.cpp, and
+// waits only for the data its next instruction consumes (arXiv 2609.12379 Sec. 4.1).
+#pragma once
+#include "fm_device.h"
+#include "fm_ops.h"
+
+namespace fm {
+namespace dev {
+
+template <int B, int D, int GT>
+__global__ __launch_bounds__(NT, 1) void step_kernel(const Params* __restrict__ pparams, Step st) {
+  CParams& p = *(CParams*)pparams;
+  __shared__ __attribute__((aligned(16))) float smem[LDS_FLOATS];
+  const int tid = threadIdx.x, lane = tid & 63, wg = blockIdx.x;
+  // The wave index is uniform across a wave; readfirstlane tells the compiler so, which keeps
+  // per-wave loop counters and buffer descriptors in scalar registers.
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // Per-lane inputs live on the device: check them here. A bad step does nothing but record
+  // the error (every workgroup reaches the same verdict).
+  u32 code = 0;
+  if (tid < p.b) {
+    const int t = st.tok[tid], ps = st.pos[tid], kl = st.kvl[tid];
+    if (t < 0 || t >= p.V) code = FM_DEV_BAD_TOKEN;
+    else if (ps < 0 || ps >= p.max_ctx) code = FM_DEV_BAD_POSITION;
+    else if (kl < 0 || kl >= p.max_ctx) code = FM_DEV_BAD_KV_LEN;
+  }
+  if (__syncthreads_or(code != 0)) {
+    if (code && wg == 0) raise_error(p, code);
+    return;
+  }
+  if (abort_raised(p)) return;
+
+  int q0, q1;
+  if (st.stage < 0) {
+    q0 = p.qoff[wg];
+    q1 = p.qoff[wg + 1];
+  } else {
+    q0 = p.stage_rng[((size_t)st.stage * p.nwg + wg) * 2];
+    q1 = p.stage_rng[((size_t)st.stage * p.nwg + wg) * 2 + 1];
+  }
+  for (int q = q0; q < q1; ++q) {
+    // Re-derive the parameter pointer per instruction, opaquely: the compiler then reloads
+    // fields from the (scalar-cached) kernel-argument segment inside each operator instead of
+    // keeping every field of every operator live in scalar registers for the whole step.
+    CParams* pp = (CParams*)pparams;
+    asm volatile("" : "+s"(pp));
+    CParams& P = *pp;
+    const int32_t* ins = P.instrs + 4 * (size_t)q;
+    const int op = ins[0];
+    u64* tl = st.timeline ? st.timeline + 8 * (size_t)q : nullptr;
+    if (tl && tid == 0) { tl[0] = clock_now(); tl[1] = 0; tl[2] = 0; tl[3] = 0; tl[5] = (u64)wg; }
+    bool ok = true;
+    if (op == FM_OP_ATTN) {
+      ok = op_attn<D, GT>(P, st, ins, smem, tid, lane, wave, tl);
+    } else if (op == FM_OP_COMBINE) {
+      ok = op_combine<D>(P, st, ins, smem, tid, lane, wave, tl);
+    } else if (op == FM_OP_GU) {
+      ok = op_gemv<B, 2>(P, st, ins, smem, tid, lane, wave, tl);
+    } else {
+      ok = op_gemv<B, 1>(P, st, ins, smem, tid, lane, wave, tl);
+    }
+    if (!ok) return;
+    if (tl && tid == 0) tl[4] = clock_now();
+  }
+}
+
+}  // namespace dev
+}  // namespace fm
+
+
+namespace fm {
+namespace dev {
+// Kernel lookup, one per batch specialisation (defined in fm_kernels.hip, compiled once per B).
+const void* kernel_for_b1(int d, int G);
+const void* kernel_for_b2(int d, int G);
+const void* kernel_for_b4(int d, int G);
+const void* kernel_for_b8(int d, int G);
+}  // namespace dev
+}  // namespace fm

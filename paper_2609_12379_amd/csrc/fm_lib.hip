@@ -1,9 +1,6 @@
-// The decode-step library: persistent interpreter kernel, multi-launch ablation and C ABI.
-//
-// One launch runs the whole step (arXiv 2609.12379 Sec. 4.1): each of the nwg workgroups
-// walks its own instruction queue, built on the host by fm_plan.cpp, and waits only for the
-// data its next instruction consumes. The multi-launch ablation runs the same kernel once
-// per stage, where stage = one operator of one layer.
+// The decode-step library's C ABI: handle creation, the single-launch step, the multi-launch
+// ablation (the same kernel launched once per stage = one operator of one layer), taps and
+// the instruction timeline. The kernels are in fm_kernel.h / fm_kernels.hip.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -14,63 +11,8 @@
 #include <vector>
 
 #include "../../include/fm.h"
-#include "fm_device.h"
-#include "fm_ops.h"
+#include "fm_kernel.h"
 #include "fm_plan.h"
-
-namespace fm {
-namespace dev {
-
-template <int B, int D>
-__global__ __launch_bounds__(NT, 1) void step_kernel(Params p) {
-  __shared__ __attribute__((aligned(16))) float smem[LDS_FLOATS];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wg = blockIdx.x;
-
-  // Per-lane inputs live on the device: check them here. A bad step does nothing but record
-  // the error (every workgroup reaches the same verdict).
-  u32 code = 0;
-  if (tid < p.b) {
-    const int t = p.tok[tid], ps = p.pos[tid], kl = p.kvl[tid];
-    if (t < 0 || t >= p.V) code = FM_DEV_BAD_TOKEN;
-    else if (ps < 0 || ps >= p.max_ctx) code = FM_DEV_BAD_POSITION;
-    else if (kl < 0 || kl >= p.max_ctx) code = FM_DEV_BAD_KV_LEN;
-  }
-  if (__syncthreads_or(code != 0)) {
-    if (code && wg == 0) raise_error(p, code);
-    return;
-  }
-  if (abort_raised(p)) return;
-
-  int q0, q1;
-  if (p.stage < 0) {
-    q0 = p.qoff[wg];
-    q1 = p.qoff[wg + 1];
-  } else {
-    q0 = p.stage_rng[((size_t)p.stage * p.nwg + wg) * 2];
-    q1 = p.stage_rng[((size_t)p.stage * p.nwg + wg) * 2 + 1];
-  }
-  for (int q = q0; q < q1; ++q) {
-    const int32_t* ins = p.instrs + 4 * (size_t)q;
-    const int op = ins[0];
-    bool ok = true;
-    if (op == FM_OP_ATTN) {
-      switch (p.G) {
-        case 1: ok = op_attn<D, 1>(p, ins, smem, tid, lane, wave); break;
-        case 2: ok = op_attn<D, 2>(p, ins, smem, tid, lane, wave); break;
-        case 3: case 4: ok = op_attn<D, 4>(p, ins, smem, tid, lane, wave); break;
-        default: ok = op_attn<D, 8>(p, ins, smem, tid, lane, wave); break;
-      }
-    } else if (op == FM_OP_GU) {
-      ok = op_gemv<B, 2>(p, ins, smem, tid, lane, wave);
-    } else {
-      ok = op_gemv<B, 1>(p, ins, smem, tid, lane, wave);
-    }
-    if (!ok) return;
-  }
-}
-
-}  // namespace dev
-}  // namespace fm
 
 using namespace fm;
 using namespace fm::dev;
@@ -82,15 +24,18 @@ struct fm_handle {
   const void* kernel = nullptr;
   int B = 1;
   Params base{};
+  Params* d_params = nullptr;
+  float* taps = nullptr;
+  u64* timeline = nullptr;
   LayerPtrs* d_layers = nullptr;
   float* d_rope = nullptr;
   int32_t *d_instrs = nullptr, *d_qoff = nullptr, *d_stage = nullptr;
   u64* d_act = nullptr;
-  float* d_part = nullptr;
-  u32* d_arrive = nullptr;
+  u64* d_part = nullptr;
   u64* d_amax = nullptr;
   u32* d_lm_arrive = nullptr;
   u32* d_abort = nullptr;
+  uint16_t* d_zero = nullptr;
   u32* h_err = nullptr;   // pinned, device-visible
   u32* d_err = nullptr;
   u32 epoch = 0;
@@ -98,17 +43,12 @@ struct fm_handle {
 
 namespace {
 
-template <int B>
-const void* pick_kernel(int d) {
-  return d == 64 ? (const void*)&step_kernel<B, 64> : (const void*)&step_kernel<B, 128>;
-}
-
-const void* kernel_for(int Bt, int d) {
+const void* kernel_for(int Bt, int d, int G) {
   switch (Bt) {
-    case 1: return pick_kernel<1>(d);
-    case 2: return pick_kernel<2>(d);
-    case 4: return pick_kernel<4>(d);
-    default: return pick_kernel<8>(d);
+    case 1: return kernel_for_b1(d, G);
+    case 2: return kernel_for_b2(d, G);
+    case 4: return kernel_for_b4(d, G);
+    default: return kernel_for_b8(d, G);
   }
 }
 
@@ -117,8 +57,8 @@ int round_batch(int b) { return b <= 1 ? 1 : b <= 2 ? 2 : b <= 4 ? 4 : 8; }
 void free_handle(fm_handle* h) {
   if (!h) return;
   hipFree(h->d_layers); hipFree(h->d_rope); hipFree(h->d_instrs); hipFree(h->d_qoff);
-  hipFree(h->d_stage); hipFree(h->d_act); hipFree(h->d_part); hipFree(h->d_arrive);
-  hipFree(h->d_amax); hipFree(h->d_lm_arrive); hipFree(h->d_abort);
+  hipFree(h->d_stage); hipFree(h->d_act); hipFree(h->d_part);
+  hipFree(h->d_amax); hipFree(h->d_lm_arrive); hipFree(h->d_abort); hipFree(h->d_params); hipFree(h->d_zero);
   if (h->h_err) hipHostFree(h->h_err);
   delete h;
 }
@@ -156,18 +96,19 @@ fm_status launch(fm_handle* h, const int32_t* tok, const int32_t* pos, const int
   if (!tok || !pos || !kvl || !next_ids) return FM_ERR_INVALID_ARG;
   if (__atomic_load_n(h->h_err, __ATOMIC_ACQUIRE) != 0) return FM_ERR_DEVICE;
   if (++h->epoch == 0) h->epoch = 1;
-  Params p = h->base;
-  p.tok = tok; p.pos = pos; p.kvl = kvl; p.logits = logits; p.next_ids = next_ids;
-  p.epoch = h->epoch;
+  Step st{};
+  st.tok = tok; st.pos = pos; st.kvl = kvl; st.logits = logits; st.next_ids = next_ids;
+  st.taps = h->taps; st.timeline = h->timeline; st.epoch = h->epoch;
+  const Params* dp = h->d_params;
   if (!multi) {
-    p.stage = -1;
-    void* args[] = {&p};
+    st.stage = -1;
+    void* args[] = {&dp, &st};
     if (hipLaunchCooperativeKernel(h->kernel, dim3(h->plan.nwg), dim3(NT), args, 0, stream) != hipSuccess)
       return FM_ERR_HIP;
   } else {
     for (int s = 0; s < h->plan.n_stages; ++s) {
-      p.stage = s;
-      void* args[] = {&p};
+      st.stage = s;
+      void* args[] = {&dp, &st};
       if (hipLaunchKernel(h->kernel, dim3(h->plan.nwg), dim3(NT), args, 0, stream) != hipSuccess)
         return FM_ERR_HIP;
     }
@@ -258,16 +199,22 @@ fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_k
     // Per-tile LDS needs: residual rows, and per-row partials when K spans several slabs.
     auto rows_max = [&](int64_t n) { return (n + nwg - 1) / nwg; };
     if (rows_max(hd) * Bt > RESID_FLOATS) { free_handle(h); return FM_ERR_CAPACITY; }
-    const int64_t ks = (XSLAB_FLOATS / Bt) & ~511;
-    auto needs = [&](int64_t K, int64_t rows, int nw) { return K > ks ? rows_max(rows) * nw * Bt : 0; };
-    if (needs(hd, nqkv, 1) > ROWACC_FLOATS || needs(nh * d, hd, 1) > ROWACC_FLOATS ||
-        needs(hd, inter, 2) > ROWACC_FLOATS || needs(inter, hd, 1) > ROWACC_FLOATS ||
-        needs(hd, V, 1) > ROWACC_FLOATS) {
+    // rowacc holds [KP][rows][nw][B]; KP > 1 only when the tile has fewer than NWAVE quads.
+    auto needs = [&](int64_t rows, int nw) {
+      const int64_t r = rows_max(rows), quads = (r * nw + 3) / 4;
+      const int64_t kp = quads < NWAVE ? NWAVE / std::max<int64_t>(quads, 1) : 1;
+      return r * nw * Bt * kp;
+    };
+    if (needs(nqkv, 1) > ROWACC_FLOATS || needs(hd, 1) > ROWACC_FLOATS || needs(inter, 2) > ROWACC_FLOATS ||
+        needs(V, 1) > ROWACC_FLOATS) {
       free_handle(h);
       return FM_ERR_CAPACITY;
     }
   }
-  h->kernel = kernel_for(Bt, (int)d);
+  // The combine stages one group's partials in LDS: G heads x chunks x (d + 2) floats.
+  if ((nh / nkv) * (int64_t)P.attn_max_chunks * (d + 2) > XSLAB_FLOATS) { free_handle(h); return FM_ERR_CAPACITY; }
+  h->kernel = kernel_for(Bt, (int)d, (int)(nh / nkv));
+  if (!h->kernel) { free_handle(h); return FM_ERR_UNSUPPORTED; }
   int occ = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, h->kernel, NT, 0) != hipSuccess) { free_handle(h); return FM_ERR_HIP; }
   if ((int64_t)occ * prop.multiProcessorCount < nwg) { free_handle(h); return FM_ERR_CAPACITY; }
@@ -300,15 +247,16 @@ fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_k
   HIP_TRY(upload(&h->d_stage, P.stage_rng.data(), P.stage_rng.size()));
   HIP_TRY(hipMalloc(&h->d_act, words * 8));
   HIP_TRY(hipMemset(h->d_act, 0, words * 8));
-  const size_t part_floats = (size_t)b * nh * P.attn_max_chunks * (d + 2);
-  HIP_TRY(hipMalloc(&h->d_part, part_floats * 4));
-  HIP_TRY(hipMemset(h->d_part, 0, part_floats * 4));
-  HIP_TRY(hipMalloc(&h->d_arrive, b * nkv * 4));
-  HIP_TRY(hipMemset(h->d_arrive, 0, b * nkv * 4));
+  const size_t part_words = (size_t)L * b * nh * P.attn_max_chunks * (d + 2);
+  if (part_words * 8 >= (1ull << 32)) { free_handle(h); return FM_ERR_CAPACITY; }
+  HIP_TRY(hipMalloc(&h->d_part, part_words * 8));
+  HIP_TRY(hipMemset(h->d_part, 0, part_words * 8));
   HIP_TRY(hipMalloc(&h->d_amax, b * 8));
   HIP_TRY(hipMemset(h->d_amax, 0, b * 8));
   HIP_TRY(hipMalloc(&h->d_lm_arrive, 64));
   HIP_TRY(hipMemset(h->d_lm_arrive, 0, 64));
+  HIP_TRY(hipMalloc(&h->d_zero, 65536));
+  HIP_TRY(hipMemset(h->d_zero, 0, 65536));
   HIP_TRY(hipMalloc(&h->d_abort, 64));
   HIP_TRY(hipMemset(h->d_abort, 0, 64));
   HIP_TRY(hipHostMalloc((void**)&h->h_err, 64, hipHostMallocMapped));
@@ -327,7 +275,7 @@ fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_k
   p.final_norm = (const uint16_t*)w->final_norm;
   p.lm_head = (const uint16_t*)(c.tied_embedding ? w->embed : w->lm_head);
   p.rope = h->d_rope;
-  p.instrs = h->d_instrs; p.qoff = h->d_qoff; p.stage_rng = h->d_stage; p.stage = -1;
+  p.instrs = h->d_instrs; p.qoff = h->d_qoff; p.stage_rng = h->d_stage;
   p.act = h->d_act; p.act_bytes = (u32)(words * 8);
   p.st_x = (u32)(b * hd); p.st_qkv = (u32)(b * nqkv); p.st_o = (u32)(b * nh * d);
   p.st_x1 = (u32)(b * hd); p.st_m = (u32)(b * inter);
@@ -336,13 +284,15 @@ fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_k
   p.off_o = p.off_qkv + (u32)L * p.st_qkv;
   p.off_x1 = p.off_o + (u32)L * p.st_o;
   p.off_m = p.off_x1 + (u32)L * p.st_x1;
-  p.part = h->d_part; p.arrive = h->d_arrive; p.amax = h->d_amax; p.lm_arrive = h->d_lm_arrive;
+  p.zero_page = h->d_zero;
+  p.part = h->d_part; p.amax = h->d_amax; p.lm_arrive = h->d_lm_arrive;
   p.abort_flag = h->d_abort; p.err_host = h->d_err;
   const TapOff t = tap_offsets(c);
-  p.taps = nullptr; p.tap_block = t.block;
+  p.tap_block = t.block;
   p.tap_a = (int32_t)t.a; p.tap_qkv = (int32_t)t.qkv; p.tap_qrot = (int32_t)t.qrot; p.tap_krot = (int32_t)t.krot;
   p.tap_o = (int32_t)t.o; p.tap_x1 = (int32_t)t.x1; p.tap_a2 = (int32_t)t.a2; p.tap_mlp = (int32_t)t.mlp;
   p.tap_x2 = (int32_t)t.x2;
+  HIP_TRY(upload(&h->d_params, &h->base, 1));
   *out = h;
   return FM_OK;
 }
@@ -372,9 +322,17 @@ fm_status fm_last_error(fm_handle* h, int32_t* device_code) {
   return *device_code ? FM_ERR_DEVICE : FM_OK;
 }
 
+fm_status fm_set_timeline(fm_handle* h, uint64_t* buf) {
+  if (!h) return FM_ERR_INVALID_ARG;
+  h->timeline = buf;
+  return FM_OK;
+}
+
+int32_t fm_instruction_count(const fm_handle* h) { return h ? (int32_t)h->plan.instrs.size() : -1; }
+
 fm_status fm_set_taps(fm_handle* h, float* tap_buf) {
   if (!h) return FM_ERR_INVALID_ARG;
-  h->base.taps = tap_buf;
+  h->taps = tap_buf;
   return FM_OK;
 }
 

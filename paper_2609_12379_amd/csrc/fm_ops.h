@@ -2,6 +2,8 @@
 // prologue, residual/SiLU/argmax epilogues) and split-KV attention work items (with fused
 // QK-norm, RoPE, KV append, online softmax and a last-arriver log-sum-exp combine).
 #pragma once
+#include <type_traits>
+
 #include "fm_device.h"
 #include "../../include/fm.h"
 
@@ -10,27 +12,27 @@ namespace dev {
 
 // ---- waiting on tagged words ----------------------------------------------------------
 
-__device__ __forceinline__ bool abort_raised(const Params& p) {
+__device__ __forceinline__ bool abort_raised(CParams& p) {
   return __hip_atomic_load(p.abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
 }
 
-__device__ __forceinline__ void raise_error(const Params& p, u32 code) {
+__device__ __forceinline__ void raise_error(CParams& p, u32 code) {
   __hip_atomic_store(p.abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __hip_atomic_store(p.err_host, code, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 // Reads the tagged pair at word offset w (even), spinning until both words carry the
 // epoch. Returns false if the watchdog fires or another workgroup raised the abort flag.
-__device__ __forceinline__ bool wait_pair(const Params& p, __amdgpu_buffer_rsrc_t ra, u32 w,
+__device__ __forceinline__ bool wait_pair(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, u32 w,
                                           float& a, float& b) {
   u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(ra, w * 8u, 0, CPOL_SC1);
-  if (v.y != p.epoch || v.w != p.epoch) {
+  if (v.y != st.epoch || v.w != st.epoch) {
     const u64 t0 = clock_now();
     int it = 0;
     while (true) {
       __builtin_amdgcn_s_sleep(1);
       v = __builtin_amdgcn_raw_buffer_load_b128(ra, w * 8u, 0, CPOL_SC1);
-      if (v.y == p.epoch && v.w == p.epoch) break;
+      if (v.y == st.epoch && v.w == st.epoch) break;
       if ((++it & 63) == 0) {
         if (clock_now() - t0 > WAIT_TICKS) {
           raise_error(p, FM_DEV_WATCHDOG);
@@ -46,16 +48,76 @@ __device__ __forceinline__ bool wait_pair(const Params& p, __amdgpu_buffer_rsrc_
 }
 
 // Wait for n (even) tagged words at word offset w0 and copy their values to dst (LDS);
-// accumulates the sum of squares of the values this thread copied into ss.
-__device__ __forceinline__ bool wait_copy(const Params& p, __amdgpu_buffer_rsrc_t ra, u32 w0, int n,
+// accumulates the sum of squares of the values this thread copied into ss. Each thread
+// issues up to WB pair loads before checking any of them, so a vector costs one round trip
+// when its producers are done; stale pairs are then re-polled one by one.
+constexpr int WB = 8;
+template <int WBT = WB>
+__device__ __forceinline__ bool wait_copy_t(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, u32 w0, int n,
+                                            float* dst, float& ss, int t, int nthr) {
+  for (int k0 = t * 2; k0 < n; k0 += nthr * 2 * WBT) {
+    u32x4 v[WBT];
+#pragma unroll
+    for (int j = 0; j < WBT; ++j) {
+      const int k = k0 + j * nthr * 2;
+      v[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, (k < n) ? (w0 + (u32)k) * 8u : 0xFFFFFFF0u, 0, CPOL_SC1);
+    }
+#pragma unroll
+    for (int j = 0; j < WBT; ++j) {
+      const int k = k0 + j * nthr * 2;
+      if (k < n) {
+        float a = __uint_as_float(v[j].x), b = __uint_as_float(v[j].z);
+        if (v[j].y != st.epoch || v[j].w != st.epoch) {
+          if (!wait_pair(p, st, ra, w0 + (u32)k, a, b)) return false;
+        }
+        ss += a * a + b * b;
+        if (dst) {
+          dst[k] = a;
+          dst[k + 1] = b;
+        }
+      }
+    }
+  }
+  return true;
+}
+
+__device__ __forceinline__ bool wait_copy(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, u32 w0, int n,
                                           float* dst, float& ss, int tid) {
-  for (int k = tid * 2; k < n; k += NT * 2) {
-    float a, b;
-    if (!wait_pair(p, ra, w0 + (u32)k, a, b)) return false;
-    ss += a * a + b * b;
-    if (dst) {
-      dst[k] = a;
-      dst[k + 1] = b;
+  return wait_copy_t<WB>(p, st, ra, w0, n, dst, ss, tid, NT);
+}
+
+// Like wait_copy for three word ranges at once (one round trip when all are ready).
+__device__ __forceinline__ bool wait_copy3(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra,
+                                           u32 wa, int na, float* da, u32 wb, int nb, float* db,
+                                           u32 wc, int nc, float* dc, int tid) {
+  const int n = na + nb + nc;
+  auto where = [&](int k, u32& w, float*& d) {
+    if (k < na) { w = wa + (u32)k; d = da + k; }
+    else if (k < na + nb) { w = wb + (u32)(k - na); d = db + (k - na); }
+    else { w = wc + (u32)(k - na - nb); d = dc + (k - na - nb); }
+  };
+  for (int k0 = tid * 2; k0 < n; k0 += NT * 2 * WB) {
+    u32x4 v[WB];
+#pragma unroll
+    for (int j = 0; j < WB; ++j) {
+      const int k = k0 + j * NT * 2;
+      u32 w = 0; float* d = nullptr;
+      if (k < n) where(k, w, d);
+      v[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, (k < n) ? w * 8u : 0xFFFFFFF0u, 0, CPOL_SC1);
+    }
+#pragma unroll
+    for (int j = 0; j < WB; ++j) {
+      const int k = k0 + j * NT * 2;
+      if (k < n) {
+        u32 w; float* d;
+        where(k, w, d);
+        float a = __uint_as_float(v[j].x), b = __uint_as_float(v[j].z);
+        if (v[j].y != st.epoch || v[j].w != st.epoch) {
+          if (!wait_pair(p, st, ra, w, a, b)) return false;
+        }
+        d[0] = a;
+        d[1] = b;
+      }
     }
   }
   return true;
@@ -82,20 +144,93 @@ __device__ __forceinline__ u32 ordered(float f) {
 
 // ---- GEMV row tile ---------------------------------------------------------------------
 //
-// Output rows [ra, rb) of one operator, B lanes (B is the batch rounded up to 1, 2, 4 or 8),
-// NW weight rows per output row (2 for gate/up, else 1). Rows are dealt to the waves
-// round-robin. Inside a wave, each lane streams 16 bytes (8 bf16) per weight-row segment of
-// 512 columns. U such loads stay in flight per lane in a register ring. The ring is filled
-// BEFORE the input wait, so a tile's weights stream while its producers finish. The input
-// vector is staged in LDS (fp32, RMSNorm applied when the operator has one) in slabs of
-// at most XSLAB_FLOATS / B columns. Partial sums across slabs accumulate in LDS.
+// Output rows [ra, rb) of one operator for B lanes (B = batch rounded up to 1, 2, 4, 8), with
+// NW weight rows per output row (2 for gate/up: weight row wr = 2 q + {0: gate, 1: up}).
+//
+// Lane layout: 16 lanes per weight row, 4 rows per wave load. A load ("unit") is 16 B per lane
+// = 128 columns of each of 4 rows ("quad"), so one reduction is a 4-step DPP sum inside each
+// 16-lane row and the activation chunk is an LDS broadcast. Quads are split along K into KP
+// parts when the tile has fewer quads than waves, so every wave keeps U = 16 loads in flight
+// whatever the tile's shape. Items (quad, part) are dealt to waves round-robin; a wave's units
+// run item by item, SP segments per item. Part sums land in LDS and are added in part order
+// by the epilogue, so results do not depend on timing.
+//
+// Every ring slot issues exactly one global load (so the compiler counts loads in flight
+// exactly); lanes with nothing to load read a zeroed page instead.
+
+struct GemvGeom {
+  int K, Ks, nslab;           // columns, slab width, slabs
+  int nwr, NQ, KP, nitems;    // weight rows, quads, K parts, items
+  int nseg, SP, kend, k0;     // current slab: segments, segments per part, column bound/start
+  int items_w;                // items of this wave
+};
+
+struct GemvCursor {
+  int it, sg;                 // wave-local item and segment within it
+  int qd, pt;                 // its quad and K part
+  bool live;                  // item exists
+};
+
+// Wave-uniform integers are passed through readfirstlane so the compiler keeps them (and
+// the branches on them) scalar; otherwise the ring's loads end up under divergent control
+// flow and the compiler can no longer count them in flight.
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+__device__ __forceinline__ void cursor_at(GemvCursor& c, const GemvGeom& g, int it, int wave) {
+  c.it = uni(it); c.sg = 0;
+  const int t = uni(wave + it * NSW);
+  c.live = uni(it < g.items_w ? 1 : 0) != 0;
+  c.qd = uni(t / g.KP);
+  c.pt = uni(t - c.qd * g.KP);
+}
+
+__device__ __forceinline__ void cursor_next(GemvCursor& c, const GemvGeom& g, int wave) {
+  c.sg = uni(c.sg + 1);
+  if (c.sg == g.SP) cursor_at(c, g, c.it + 1, wave);
+}
+
+// Issues the load of the cursor's unit into `dst`. Units that do not exist (past the wave's
+// items, or past the slab's segments in a short last K part) issue nothing: a load whose
+// result is never used would still have to complete before its registers are reused.
+// Lanes of an existing unit that fall outside the matrix (rows past the tile, the ragged
+// last segment) read their zero-page slot instead.
+template <int NW>
+__device__ __forceinline__ void load_unit(u32x4& dst, const GemvGeom& g, const GemvCursor& c, int lane, int op,
+                                          int ra, const uint16_t* m0, const uint16_t* m1, const uint16_t* m2,
+                                          int n0, int n1, const uint16_t* zero_page) {
+  const int seg = c.pt * g.SP + c.sg;
+  if (!(c.live && seg < g.nseg)) return;
+  const int wr = c.qd * 4 + (lane >> 4);
+  const int k = g.k0 + seg * 128 + (lane & 15) * 8;
+  const bool valid = wr < g.nwr && k < g.kend;
+  const uint16_t* ptr;
+  if (NW == 2) {
+    ptr = ((wr & 1) ? m1 : m0) + (size_t)(ra + (wr >> 1)) * g.K + k;
+  } else {
+    const int r = ra + wr;
+    if (op == FM_OP_QKV) {
+      ptr = (r >= n0 + n1) ? m2 + (size_t)(r - n0 - n1) * g.K + k
+          : (r >= n0 ? m1 + (size_t)(r - n0) * g.K + k : m0 + (size_t)r * g.K + k);
+    } else {
+      ptr = m0 + (size_t)r * g.K + k;
+    }
+  }
+  dst = ld_stream16(valid ? ptr : zero_page);
+}
+
+// Per-lane slot in the 64 KiB zero page (16 B per lane, spread over 4096 slots so idle lanes
+// of different waves and workgroups do not all hit one cache line).
+__device__ __forceinline__ const uint16_t* zero_slot(CParams& p, int wave, int lane) {
+  return p.zero_page + ((((int)blockIdx.x * NWAVE + wave) * 64 + lane) & 4095) * 8;
+}
 
 template <int B, int NW>
-__device__ bool op_gemv(const Params& p, const int32_t* ins, float* smem, int tid, int lane, int wave) {
-  const int op = ins[0], l = ins[1], ra = ins[2], rb = ins[3];
+__device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_t* ins, float* smem, int tid,
+                                        int lane, int wave, u64* tl) {
+  const int op = uni(ins[0]), l = uni(ins[1]), ra = uni(ins[2]), rb = uni(ins[3]);
   const int nr = rb - ra;
   const int nq = p.nh * p.d, nk = p.nkv * p.d, nqkv = nq + 2 * nk;
-  const LayerPtrs* Lw = (op == FM_OP_LM) ? nullptr : p.layers + l;
+  CLayerPtrs* Lw = (op == FM_OP_LM) ? nullptr : (CLayerPtrs*)p.layers + l;
 
   // Operator geometry.
   int K = 0;
@@ -105,12 +240,11 @@ __device__ bool op_gemv(const Params& p, const int32_t* ins, float* smem, int ti
   u32 res_w = 0, res_stride = 0;    // tagged residual (OPROJ, DOWN)
   bool res_embed = false, has_res = false;
   const uint16_t* m0 = nullptr; const uint16_t* m1 = nullptr; const uint16_t* m2 = nullptr;
-  u32 n0 = 0, n1 = 0;               // QKV: rows of W_q, W_k
   switch (op) {
     case FM_OP_QKV:
       K = p.h; gain = Lw->attn_norm;
       if (l == 0) from_embed = true; else { in_w = p.off_x + (u32)l * p.st_x; in_stride = p.h; }
-      m0 = Lw->wq; m1 = Lw->wk; m2 = Lw->wv; n0 = nq; n1 = nk;
+      m0 = Lw->wq; m1 = Lw->wk; m2 = Lw->wv;
       break;
     case FM_OP_OPROJ:
       K = nq; in_w = p.off_o + (u32)l * p.st_o; in_stride = nq;
@@ -132,124 +266,159 @@ __device__ bool op_gemv(const Params& p, const int32_t* ins, float* smem, int ti
       m0 = p.lm_head;
       break;
   }
-  const u32 rowbytes = (u32)K * 2u;
-  __amdgpu_buffer_rsrc_t r0, r1, r2;
-  if (op == FM_OP_QKV) {
-    r0 = rsrc(m0, n0 * rowbytes); r1 = rsrc(m1, n1 * rowbytes); r2 = rsrc(m2, n1 * rowbytes);
-  } else if (op == FM_OP_GU) {
-    r0 = rsrc(m0, (u32)p.inter * rowbytes); r1 = rsrc(m1, (u32)p.inter * rowbytes); r2 = r0;
-  } else {
-    const u32 rows = (op == FM_OP_LM) ? (u32)p.V : (u32)p.h;
-    r0 = rsrc(m0, rows * rowbytes); r1 = r0; r2 = r0;
-  }
   const __amdgpu_buffer_rsrc_t ract = rsrc(p.act, p.act_bytes);
 
-  // Slab geometry.
-  const int Kpad = (K + 511) & ~511;
-  int Ks = (XSLAB_FLOATS / B) & ~511;
-  if (Ks > Kpad) Ks = Kpad;
-  const int nslab = (K + Ks - 1) / Ks;
-  const int rows_w = nr > wave ? (nr - wave + NWAVE - 1) / NWAVE : 0;
+  // Geometry (all wave-uniform).
+  GemvGeom g;
+  g.K = K;
+  {
+    const int Kpad = (K + 127) & ~127;
+    int ks = (XSLAB_FLOATS / B) & ~127;
+    g.Ks = ks < Kpad ? ks : Kpad;
+  }
+  g.K = uni(K);
+  g.Ks = uni(g.Ks);
+  g.nslab = uni((K + g.Ks - 1) / g.Ks);
+  g.nwr = uni(nr * NW);
+  g.NQ = uni((g.nwr + 3) >> 2);
+  auto set_slab = [&](int s) {
+    g.k0 = uni(s * g.Ks);
+    const int kn = min(g.Ks, K - g.k0);
+    g.kend = uni(g.k0 + kn);
+    g.nseg = uni((kn + 127) >> 7);
+    int kp = 1;
+    if (g.nslab == 1 && g.NQ < NSW) {
+      kp = NSW / g.NQ;
+      if (kp > g.nseg) kp = g.nseg;
+    }
+    g.KP = uni(kp);
+    g.SP = uni((g.nseg + g.KP - 1) / g.KP);
+    g.nitems = uni(g.NQ * g.KP);
+    g.items_w = uni((wave < NSW && g.nitems > wave) ? (g.nitems - wave + NSW - 1) / NSW : 0);
+  };
+  set_slab(0);
+  const int KP0 = g.KP;
 
   float* xs = smem;
-  float* rowacc = smem + XSLAB_FLOATS;
+  float* rowacc = smem + XSLAB_FLOATS;   // [KP][nr][NW][B]
   float* resid = rowacc + ROWACC_FLOATS;
   float* misc = resid + RESID_FLOATS;
 
-  // Weight ring: deeper for small batches (fewer accumulators, more registers free).
-  constexpr int U = (B <= 2) ? 16 : 8;
+  // 1. Prefetch the first U units (and the RMSNorm gains), before waiting for the input.
+  const uint16_t* zp = zero_slot(p, wave, lane);
+  constexpr int U = FM_RING;
   u32x4 ring[U];
-  int iq = 0, iw = 0, isg = 0;   // next unit to issue: (row of this wave, weight row, segment)
-  int slab_i = 0, nseg_i = 0;    // slab being issued and its segment count
-  auto seg_count = [&](int s) { return (min(Ks, K - s * Ks) + 511) >> 9; };
-  auto issue = [&](int slot) {
-    u32 off = 0xFFFFFFF0u;       // past every resource: the load returns zeros, no traffic
-    __amdgpu_buffer_rsrc_t rr = r0;
-    if (iq < rows_w) {
-      const int r = ra + wave + iq * NWAVE;
-      const int k = slab_i * Ks + isg * 512 + lane * 8;
-      u32 lrow = (u32)r;
-      if (op == FM_OP_QKV) {
-        if (r >= (int)(n0 + n1)) { rr = r2; lrow = (u32)r - n0 - n1; }
-        else if (r >= (int)n0) { rr = r1; lrow = (u32)r - n0; }
-      } else if (NW == 2 && iw == 1) {
-        rr = r1;
-      }
-      if (k < K) off = lrow * rowbytes + (u32)k * 2u;
-      if (++isg == nseg_i) { isg = 0; if (++iw == NW) { iw = 0; ++iq; } }
-    }
-    ring[slot] = __builtin_amdgcn_raw_buffer_load_b128(rr, off, 0, CPOL_NT);
-  };
-  auto start_slab_issue = [&](int s) {
-    slab_i = s; nseg_i = seg_count(s); iq = 0; iw = 0; isg = 0;
+  GemvCursor ci;                          // issue cursor
+  cursor_at(ci, g, 0, wave);
 #pragma unroll
-    for (int sl = 0; sl < U; ++sl) issue(sl);
-  };
+  for (int sl = 0; sl < U; ++sl) {
+    load_unit<NW>(ring[sl], g, ci, lane, op, ra, m0, m1, m2, nq, nk, zp);
+    cursor_next(ci, g, wave);
+  }
 
-  // 1. Prefetch the first weights, before waiting for the input.
-  start_slab_issue(0);
+  constexpr int GP = 8;                  // gain pairs held in registers (K <= 8192)
+  u32 gpair[GP];
+  const bool gains_in_regs = gain && g.nslab == 1 && K <= GP * NT * 2;
+#pragma unroll
+  for (int jj = 0; jj < GP; ++jj) {
+    const int k = tid * 2 + jj * NT * 2;
+    gpair[jj] = (gains_in_regs && k < K) ? *reinterpret_cast<const u32*>(gain + k) : 0u;
+  }
 
   // 2. Input: wait for the producers, then stage (normalised) values in LDS.
   bool ok = true;
   float rs[B];
 #pragma unroll
   for (int i = 0; i < B; ++i) rs[i] = 1.0f;
+  // Inputs are polled and staged by the control waves (ct = thread index among them).
+  const bool ctl = (NCTL == 0) || wave >= NSW;
+  const int ct = NCTL ? tid - NSW * 64 : tid, nct = NCTL ? NCTL * 64 : NT;
   auto stage = [&](int s, bool accumulate_ss, float* ssv) -> bool {
-    const int k0 = s * Ks, kn = min(Ks, K - k0);
-    const int kfill = (kn + 511) & ~511;
+    const int k0 = s * g.Ks, kn = min(g.Ks, K - k0);
+    const int kfill = (kn + 127) & ~127;
 #pragma unroll
     for (int i = 0; i < B; ++i) {
-      float* dst = xs + i * Ks;
-      float ss = 0.f;
-      if (i < p.b) {
-        if (from_embed) {
-          const uint16_t* e = p.embed + (size_t)p.tok[i] * p.h + k0;
-          for (int k = tid * 2; k < kn; k += NT * 2) {
-            u32 w2 = *reinterpret_cast<const u32*>(e + k);
-            float a = bf16lo(w2), b = bf16hi(w2);
-            ss += a * a + b * b;
-            dst[k] = a; dst[k + 1] = b;
-          }
-        } else {
-          if (!wait_copy(p, ract, in_w + (u32)i * in_stride + (u32)k0, kn, dst, ss, tid)) return false;
-        }
-      } else {
+      float* dst = xs + i * g.Ks;
+      // zero padding (and absent batch lanes): any thread, disjoint from staged columns
+      if (i >= p.b) {
         for (int k = tid; k < kn; k += NT) dst[k] = 0.f;
       }
       for (int k = kn + tid; k < kfill; k += NT) dst[k] = 0.f;
-      if (accumulate_ss) ssv[i] += ss;
+      if (!ctl || i >= p.b) continue;
+      float ss = 0.f;
+      if (from_embed) {
+        const uint16_t* e = p.embed + (size_t)st.tok[i] * p.h + k0;
+        for (int k = ct * 2; k < kn; k += nct * 2) {
+          u32 w2 = *reinterpret_cast<const u32*>(e + k);
+          float a = bf16lo(w2), b = bf16hi(w2);
+          ss += a * a + b * b;
+          dst[k] = a; dst[k + 1] = b;
+        }
+      } else {
+        if (!wait_copy_t<WB>(p, st, ract, in_w + (u32)i * in_stride + (u32)k0, kn, dst, ss, ct, nct)) return false;
+      }
+      if (accumulate_ss) {
+#pragma unroll
+        for (int ii = 0; ii < B; ++ii) if (ii == i) ssv[ii] += ss;   // static register index
+      }
     }
     return true;
   };
   auto scale_slab = [&](int s) {
     if (!gain) return;
-    const int k0 = s * Ks, kn = min(Ks, K - k0);
+    if (gains_in_regs) {
+#pragma unroll
+      for (int i = 0; i < B; ++i) {
+        float* dst = xs + i * g.Ks;
+#pragma unroll
+        for (int jj = 0; jj < GP; ++jj) {
+          const int k = tid * 2 + jj * NT * 2;
+          if (k < K) {
+            dst[k] = dst[k] * rs[i] * bf16lo(gpair[jj]);
+            dst[k + 1] = dst[k + 1] * rs[i] * bf16hi(gpair[jj]);
+          }
+        }
+      }
+      return;
+    }
+    const int k0 = s * g.Ks, kn = min(g.Ks, K - k0);
 #pragma unroll
     for (int i = 0; i < B; ++i) {
-      float* dst = xs + i * Ks;
+      float* dst = xs + i * g.Ks;
       for (int k = tid; k < kn; k += NT) dst[k] = dst[k] * rs[i] * __uint_as_float((u32)gain[k0 + k] << 16);
+    }
+  };
+  auto tap_slab = [&](int s) {
+    if (!(st.taps && gain && ra == 0)) return;
+    const int k0 = s * g.Ks, kn = min(g.Ks, K - k0);
+    const int off = (op == FM_OP_QKV) ? p.tap_a : (op == FM_OP_GU ? p.tap_a2 : 0);
+    for (int i = 0; i < p.b; ++i) {
+      float* t = (op == FM_OP_LM)
+                     ? st.taps + (size_t)p.L * p.b * p.tap_block + (size_t)i * p.h
+                     : st.taps + ((size_t)l * p.b + i) * p.tap_block + off;
+      for (int k = tid; k < kn; k += NT) t[k0 + k] = xs[i * g.Ks + k];
     }
   };
 
   float ssv[B];
 #pragma unroll
   for (int i = 0; i < B; ++i) ssv[i] = 0.f;
-  if (nslab == 1) {
+  if (g.nslab == 1) {
     ok = stage(0, gain != nullptr, ssv);
   } else if (gain) {
     // Whole-vector pass for the norm statistics, then stage slab 0.
     for (int i = 0; i < B && ok; ++i) {
-      if (i >= p.b) continue;
+      if (i >= p.b || !ctl) continue;
       float ss = 0.f;
       if (from_embed) {
-        const uint16_t* e = p.embed + (size_t)p.tok[i] * p.h;
-        for (int k = tid * 2; k < K; k += NT * 2) {
+        const uint16_t* e = p.embed + (size_t)st.tok[i] * p.h;
+        for (int k = ct * 2; k < K; k += nct * 2) {
           u32 w2 = *reinterpret_cast<const u32*>(e + k);
           float a = bf16lo(w2), b = bf16hi(w2);
           ss += a * a + b * b;
         }
       } else {
-        ok = wait_copy(p, ract, in_w + (u32)i * in_stride, K, nullptr, ss, tid);
+        ok = wait_copy_t<WB>(p, st, ract, in_w + (u32)i * in_stride, K, nullptr, ss, ct, nct);
       }
       ssv[i] += ss;
     }
@@ -258,18 +427,17 @@ __device__ bool op_gemv(const Params& p, const int32_t* ins, float* smem, int ti
     ok = stage(0, false, ssv);
   }
   // Residual rows for the epilogue.
-  if (ok && has_res) {
+  if (ok && has_res && ctl) {
     for (int i = 0; i < B && ok; ++i) {
       if (i >= p.b) continue;
       if (res_embed) {
-        const uint16_t* e = p.embed + (size_t)p.tok[i] * p.h;
-        for (int k = tid; k < nr; k += NT) resid[i * nr + k] = __uint_as_float((u32)e[ra + k] << 16);
+        const uint16_t* e = p.embed + (size_t)st.tok[i] * p.h;
+        for (int k = ct; k < nr; k += nct) resid[i * nr + k] = __uint_as_float((u32)e[ra + k] << 16);
       } else {
-        // ra is even for every split (rows are split into even-sized... not guaranteed): copy pairwise from an even base
         const int lo = ra & ~1, hi = (rb + 1) & ~1;
-        for (int k = lo + tid * 2; k < hi; k += NT * 2) {
+        for (int k = lo + ct * 2; k < hi; k += nct * 2) {
           float a, b;
-          if (!wait_pair(p, ract, res_w + (u32)i * res_stride + (u32)k, a, b)) { ok = false; break; }
+          if (!wait_pair(p, st, ract, res_w + (u32)i * res_stride + (u32)k, a, b)) { ok = false; break; }
           if (k >= ra && k < rb) resid[i * nr + (k - ra)] = a;
           if (k + 1 >= ra && k + 1 < rb) resid[i * nr + (k + 1 - ra)] = b;
         }
@@ -277,6 +445,7 @@ __device__ bool op_gemv(const Params& p, const int32_t* ins, float* smem, int ti
     }
   }
   if (__syncthreads_or(!ok)) return false;
+  if (tl && tid == 0) tl[1] = clock_now();
   if (gain) {
 #pragma unroll
     for (int i = 0; i < B; ++i) {
@@ -286,30 +455,11 @@ __device__ bool op_gemv(const Params& p, const int32_t* ins, float* smem, int ti
     scale_slab(0);
     __syncthreads();
   }
-  // Taps of the normed input (first tile of the operator only), one slab at a time.
-  auto tap_slab = [&](int s) {
-    if (!(p.taps && gain && ra == 0)) return;
-    const int k0 = s * Ks, kn = min(Ks, K - k0);
-    const int off = (op == FM_OP_QKV) ? p.tap_a : (op == FM_OP_GU ? p.tap_a2 : 0);
-    for (int i = 0; i < p.b; ++i) {
-      float* t = (op == FM_OP_LM)
-                     ? p.taps + (size_t)p.L * p.b * p.tap_block + (size_t)i * p.h
-                     : p.taps + ((size_t)l * p.b + i) * p.tap_block + off;
-      for (int k = tid; k < kn; k += NT) t[k0 + k] = xs[i * Ks + k];
-    }
-  };
   tap_slab(0);
+  if (tl && tid == 0) tl[2] = clock_now();
 
-  // 3. Stream the weights.
-  float best_v[B];
-  int best_i[B];
-#pragma unroll
-  for (int i = 0; i < B; ++i) { best_v[i] = 0.f; best_i[i] = -1; }
-  float v0[B];
-#pragma unroll
-  for (int i = 0; i < B; ++i) v0[i] = 0.f;
-
-  for (int s = 0; s < nslab; ++s) {
+  // 3. Stream the weights: consume the ring in order, refilling each slot as it is used.
+  for (int s = 0; s < g.nslab; ++s) {
     if (s > 0) {
       __syncthreads();
       if (!stage(s, false, ssv)) ok = false;
@@ -317,144 +467,149 @@ __device__ bool op_gemv(const Params& p, const int32_t* ins, float* smem, int ti
       scale_slab(s);
       __syncthreads();
       tap_slab(s);
-      start_slab_issue(s);
-    }
-    const int nseg = seg_count(s);
-    const int units = rows_w * NW * nseg;
-    int cq = 0, cw = 0, csg = 0;
-    float acc0[B], acc1[B];
+      set_slab(s);
+      cursor_at(ci, g, 0, wave);
 #pragma unroll
-    for (int i = 0; i < B; ++i) { acc0[i] = 0.f; acc1[i] = 0.f; }
+      for (int sl = 0; sl < U; ++sl) {
+        load_unit<NW>(ring[sl], g, ci, lane, op, ra, m0, m1, m2, nq, nk, zp);
+        cursor_next(ci, g, wave);
+      }
+    }
+    const int units = uni(g.items_w * g.SP);
+    GemvCursor cc;                        // consume cursor
+    cursor_at(cc, g, 0, wave);
+    float acc[B];
+#pragma unroll
+    for (int i = 0; i < B; ++i) acc[i] = 0.f;
     for (int base = 0; base < units; base += U) {
 #pragma unroll
       for (int sl = 0; sl < U; ++sl) {
         if (base + sl < units) {
           const u32x4 w = ring[sl];
-          issue(sl);
-          const float wf[8] = {bf16lo(w.x), bf16hi(w.x), bf16lo(w.y), bf16hi(w.y),
-                               bf16lo(w.z), bf16hi(w.z), bf16lo(w.w), bf16hi(w.w)};
-          const int kk = csg * 512 + lane * 8;
-#pragma unroll
-          for (int i = 0; i < B; ++i) {
-            const float4 xa = *reinterpret_cast<const float4*>(xs + i * Ks + kk);
-            const float4 xb = *reinterpret_cast<const float4*>(xs + i * Ks + kk + 4);
-            float t0 = wf[0] * xa.x, t1 = wf[1] * xa.y;
-            t0 = fmaf(wf[2], xa.z, t0); t1 = fmaf(wf[3], xa.w, t1);
-            t0 = fmaf(wf[4], xb.x, t0); t1 = fmaf(wf[5], xb.y, t1);
-            t0 = fmaf(wf[6], xb.z, t0); t1 = fmaf(wf[7], xb.w, t1);
-            if (NW == 2 && cw == 1) acc1[i] += t0 + t1; else acc0[i] += t0 + t1;
-          }
-          if (csg == nseg - 1) {
-            // One weight row finished for this slab: reduce across the wave.
-            float v[B];
+          load_unit<NW>(ring[sl], g, ci, lane, op, ra, m0, m1, m2, nq, nk, zp);
+          cursor_next(ci, g, wave);
+          const int seg = cc.pt * g.SP + cc.sg;
+          // Units past the slab's segments (the last K part may be short) were never loaded
+          // and contribute nothing.
+          if (seg < g.nseg) {
+            const int kk = seg * 128 + (lane & 15) * 8;   // column within the slab
+            const float w0 = bf16lo(w.x), w1 = bf16hi(w.x), w2 = bf16lo(w.y), w3 = bf16hi(w.y);
+            const float w4 = bf16lo(w.z), w5 = bf16hi(w.z), w6 = bf16lo(w.w), w7 = bf16hi(w.w);
 #pragma unroll
             for (int i = 0; i < B; ++i) {
-              v[i] = wave_sum((NW == 2 && cw == 1) ? acc1[i] : acc0[i]);
-              if (NW == 2 && cw == 1) acc1[i] = 0.f; else acc0[i] = 0.f;
+              const float4 xa = *reinterpret_cast<const float4*>(xs + i * g.Ks + kk);
+              const float4 xb = *reinterpret_cast<const float4*>(xs + i * g.Ks + kk + 4);
+              float t0 = w0 * xa.x, t1 = w1 * xa.y;
+              t0 = fmaf(w2, xa.z, t0); t1 = fmaf(w3, xa.w, t1);
+              t0 = fmaf(w4, xb.x, t0); t1 = fmaf(w5, xb.y, t1);
+              t0 = fmaf(w6, xb.z, t0); t1 = fmaf(w7, xb.w, t1);
+              acc[i] += t0 + t1;
             }
-            const int rl = wave + cq * NWAVE;   // row within the tile
-            if (nslab > 1) {
-              float* ra_ = rowacc + (rl * NW + cw) * B;
+          }
+          if (cc.sg == g.SP - 1) {
+            // Item finished: each 16-lane row sums its weight row; its first lane stores the
+            // part sum (added to earlier slabs' sums).
+            const int wr = cc.qd * 4 + (lane >> 4);
+            const bool writer = (lane & 15) == 0 && wr < g.nwr;
 #pragma unroll
-              for (int i = 0; i < B; ++i) {
-                const float prev = (s == 0) ? 0.f : ra_[i];
-                v[i] += prev;
-              }
-              if (s < nslab - 1) {
-                if (lane == 0) {
-#pragma unroll
-                  for (int i = 0; i < B; ++i) ra_[i] = v[i];
-                }
-              }
-            }
-            if (s == nslab - 1) {
-              if (NW == 2 && cw == 0) {
-#pragma unroll
-                for (int i = 0; i < B; ++i) v0[i] = v[i];
-              } else {
-                // Epilogue for output row r.
-                const int r = ra + rl;
-                if (lane == 0) {
-#pragma unroll
-                  for (int i = 0; i < B; ++i) {
-                    if (i >= p.b) break;
-                    float y = v[i];
-                    switch (op) {
-                      case FM_OP_QKV:
-                        st_tag(p.act + p.off_qkv + (u32)l * p.st_qkv + (u32)i * nqkv + r, y, p.epoch);
-                        if (p.taps) p.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_qkv + r] = y;
-                        break;
-                      case FM_OP_OPROJ:
-                        y += resid[i * nr + rl];
-                        st_tag(p.act + p.off_x1 + (u32)l * p.st_x1 + (u32)i * p.h + r, y, p.epoch);
-                        if (p.taps) p.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_x1 + r] = y;
-                        break;
-                      case FM_OP_GU:
-                        y = silu(v0[i]) * v[i];
-                        st_tag(p.act + p.off_m + (u32)l * p.st_m + (u32)i * p.inter + r, y, p.epoch);
-                        break;
-                      case FM_OP_DOWN: {
-                        const float xr = y + resid[i * nr + rl];
-                        st_tag(p.act + p.off_x + (u32)(l + 1) * p.st_x + (u32)i * p.h + r, xr, p.epoch);
-                        if (p.taps) {
-                          p.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_mlp + r] = y;
-                          p.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_x2 + r] = xr;
-                        }
-                        break;
-                      }
-                      default:
-                        if (p.logits) __builtin_nontemporal_store(y, p.logits + (size_t)i * p.V + r);
-                        break;
-                    }
-                  }
-                }
-                if (op == FM_OP_LM) {
-#pragma unroll
-                  for (int i = 0; i < B; ++i) {
-                    if (best_i[i] < 0 || v[i] > best_v[i]) { best_v[i] = v[i]; best_i[i] = r; }
-                  }
-                }
+            for (int i = 0; i < B; ++i) {
+              const float v = row16_sum(acc[i]);
+              acc[i] = 0.f;
+              if (writer) {
+                float* dst = rowacc + ((cc.pt * nr) * NW + wr) * B + i;
+                *dst = (s == 0) ? v : *dst + v;
               }
             }
           }
-          if (++csg == nseg) { csg = 0; if (++cw == NW) { cw = 0; ++cq; } }
+          cursor_next(cc, g, wave);
+        }
+      }
+    }
+  }
+  __syncthreads();
+  if (tl && tid == 0) tl[3] = clock_now();
+
+  // 4. Epilogue, one output row per thread: K-part sums in order, residual adds, SiLU * up,
+  //    tagged stores, taps, logits; the LM head also folds its rows into one packed argmax
+  //    key per lane.
+  u64 key[B];
+#pragma unroll
+  for (int i = 0; i < B; ++i) key[i] = 0;
+  for (int rl = tid; rl < nr; rl += NT) {
+    const int r = ra + rl;
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+      if (i >= p.b) break;
+      float y = 0.f, up = 0.f;
+      for (int pt = 0; pt < KP0; ++pt) {
+        y += rowacc[((pt * nr + rl) * NW) * B + i];
+        if (NW == 2) up += rowacc[((pt * nr + rl) * NW + 1) * B + i];
+      }
+      switch (op) {
+        case FM_OP_QKV:
+          st_tag(p.act + p.off_qkv + (u32)l * p.st_qkv + (u32)i * nqkv + r, y, st.epoch);
+          if (st.taps) st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_qkv + r] = y;
+          break;
+        case FM_OP_OPROJ: {
+          const float x1 = y + resid[i * nr + rl];
+          st_tag(p.act + p.off_x1 + (u32)l * p.st_x1 + (u32)i * p.h + r, x1, st.epoch);
+          if (st.taps) st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_x1 + r] = x1;
+          break;
+        }
+        case FM_OP_GU:
+          st_tag(p.act + p.off_m + (u32)l * p.st_m + (u32)i * p.inter + r, silu(y) * up, st.epoch);
+          break;
+        case FM_OP_DOWN: {
+          const float xr = y + resid[i * nr + rl];
+          st_tag(p.act + p.off_x + (u32)(l + 1) * p.st_x + (u32)i * p.h + r, xr, st.epoch);
+          if (st.taps) {
+            st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_mlp + r] = y;
+            st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_x2 + r] = xr;
+          }
+          break;
+        }
+        default: {
+          if (st.logits) __builtin_nontemporal_store(y, st.logits + (size_t)i * p.V + r);
+          // Packed key: order-preserving float bits, then the complemented row index, so
+          // the integer maximum picks the largest logit and, among equal ones, the lowest row.
+          const u64 k = ((u64)ordered(y) << 32) | (u64)(0xFFFFFFFFu - (u32)r);
+          key[i] = k > key[i] ? k : key[i];
+          break;
         }
       }
     }
   }
 
-  // 4. LM head: merge the waves' argmax candidates, publish one packed key per lane, and
-  //    let the last LM tile of the step write the greedy tokens.
+  // 5. LM head: one packed key per lane per tile via an integer max (order-independent),
+  //    then the last LM tile of the step writes the greedy tokens.
   if (op == FM_OP_LM) {
-    float* cand_v = misc + 16;            // [NWAVE][B]
-    int* cand_i = reinterpret_cast<int*>(misc + 16 + NWAVE * 8);
-    __syncthreads();
-    if (lane == 0) {
+    u64* wkeys = reinterpret_cast<u64*>(misc + 16);   // [NWAVE][B]
 #pragma unroll
-      for (int i = 0; i < B; ++i) { cand_v[wave * B + i] = best_v[i]; cand_i[wave * B + i] = best_i[i]; }
+    for (int i = 0; i < B; ++i) {
+      u64 k = key[i];
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) {
+        const u32 lo = __shfl_xor((u32)(k & 0xFFFFFFFFull), o, 64);
+        const u32 hi = __shfl_xor((u32)(k >> 32), o, 64);
+        const u64 ko = ((u64)hi << 32) | lo;
+        k = ko > k ? ko : k;
+      }
+      if (lane == 0) wkeys[wave * B + i] = k;
     }
     __syncthreads();
     if (tid == 0) {
       u64 sink = 0;
       for (int i = 0; i < p.b; ++i) {
-        float bv = 0.f; int bi = -1;
-        for (int w = 0; w < NWAVE; ++w) {
-          const int ci = cand_i[w * B + i];
-          const float cv = cand_v[w * B + i];
-          if (ci < 0) continue;
-          if (bi < 0 || cv > bv || (cv == bv && ci < bi)) { bv = cv; bi = ci; }
-        }
-        if (bi >= 0) {
-          const u64 key = ((u64)ordered(bv) << 32) | (u64)(0xFFFFFFFFu - (u32)bi);
-          sink += __hip_atomic_fetch_max(p.amax + i, key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
+        u64 k = 0;
+        for (int w = 0; w < NWAVE; ++w) k = wkeys[w * B + i] > k ? wkeys[w * B + i] : k;
+        if (k) sink += __hip_atomic_fetch_max(p.amax + i, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       vm_wait0();
       const u32 old = __hip_atomic_fetch_add(p.lm_arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (old + (u32)(sink == 1234567ull) == (u32)p.n_lm_instr - 1u) {
         for (int i = 0; i < p.b; ++i) {
-          const u64 key = __hip_atomic_load(p.amax + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          p.next_ids[i] = (int32_t)(0xFFFFFFFFu - (u32)(key & 0xFFFFFFFFull));
+          const u64 k = __hip_atomic_load(p.amax + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          st.next_ids[i] = (int32_t)(0xFFFFFFFFu - (u32)(k & 0xFFFFFFFFull));
           __hip_atomic_store(p.amax + i, (u64)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         __hip_atomic_store(p.lm_arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -470,24 +625,23 @@ __device__ bool op_gemv(const Params& p, const int32_t* ins, float* smem, int ti
 // Per layer the step has P work items. At run time item j maps, from kv_lens alone, to a
 // lane i, a KV head g and a chunk [t0, t1) of that lane's slots 0..kv_len: every
 // (lane, KV head) gets ceil((kv_len+1)/T) chunks of at most T slots, with T chosen so the
-// total chunk count fits in P. Ragged lanes are thus balanced per step. An item reads its
-// group's raw q (G heads), k and v and applies QK-norm and RoPE. The item holding the last
-// chunk also rounds the new k/v to bf16 and appends them at slot kv_len. The item then
-// runs an online softmax over its slots (base-2 exponent with log2(e)/sqrt(d) folded into
-// q) and publishes one partial (max, sum, weighted V) per head. The last item of a
-// (lane, KV head) to arrive merges the partials in chunk order and writes the attention
-// output.
+// total chunk count fits in P (ragged lanes are thus balanced per step). An item reads its
+// group's raw q (G heads), k and v, applies QK-norm and RoPE; the item holding the last chunk
+// also rounds the new k/v to bf16 and appends them at slot kv_len. It then runs an online
+// softmax over its slots (base-2 exponent, log2(e)/sqrt(d) folded into q) and publishes one
+// tagged partial (max, sum, weighted V) per head. A separate combine instruction per
+// (lane, KV head) waits for the partials and merges them in chunk order (log-sum-exp).
 
-__device__ __forceinline__ bool item_map(const Params& p, int j, int& i, int& g, int& c, int& nc,
+__device__ __forceinline__ bool item_map(CParams& p, const Step& st, int j, int& i, int& g, int& c, int& nc,
                                          int& t0, int& t1) {
   long long total = 0;
-  for (int ii = 0; ii < p.b; ++ii) total += p.kvl[ii] + 1;
+  for (int ii = 0; ii < p.b; ++ii) total += st.kvl[ii] + 1;
   total *= p.nkv;
   const long long denom = p.P - p.nkv * p.b;
   const int T = (int)((total + denom - 1) / denom);
   int idx = j;
   for (int ii = 0; ii < p.b; ++ii) {
-    const int W = p.kvl[ii] + 1;
+    const int W = st.kvl[ii] + 1;
     const int n = (W + T - 1) / T;
     const int per = p.nkv * n;
     if (idx < per) {
@@ -498,6 +652,16 @@ __device__ __forceinline__ bool item_map(const Params& p, int j, int& i, int& g,
     idx -= per;
   }
   return false;
+}
+
+// Chunk count of (lane i, any KV head) under the same map.
+__device__ __forceinline__ int chunks_of(CParams& p, const Step& st, int i) {
+  long long total = 0;
+  for (int ii = 0; ii < p.b; ++ii) total += st.kvl[ii] + 1;
+  total *= p.nkv;
+  const long long denom = p.P - p.nkv * p.b;
+  const int T = (int)((total + denom - 1) / denom);
+  return (st.kvl[i] + 1 + T - 1) / T;
 }
 
 __device__ __forceinline__ void sm_merge(float& m, float& l, float* acc, float mo, float lo, const float* acco) {
@@ -511,23 +675,26 @@ __device__ __forceinline__ void sm_merge(float& m, float& l, float* acc, float m
 }
 
 template <int D, int GT>
-__device__ bool op_attn(const Params& p, const int32_t* ins, float* smem, int tid, int lane, int wave) {
-  const int l = ins[1], j = ins[2];
+__device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_t* ins, float* smem, int tid,
+                                        int lane, int wave, u64* tl) {
+  const int l = uni(ins[1]), j = uni(ins[2]);
   int i, g, c, nc, t0, t1;
-  if (!item_map(p, j, i, g, c, nc, t0, t1)) return true;
+  if (!item_map(p, st, j, i, g, c, nc, t0, t1)) return true;
+  i = uni(i); g = uni(g); c = uni(c); t0 = uni(t0); t1 = uni(t1);
   const int G = p.G;
-  const int kvl = p.kvl[i];
+  const int kvl = uni(st.kvl[i]);
   const bool is_last = (t1 == kvl + 1);
   const int t_end = min(t1, kvl);            // slots [t0, t_end) come from the arena
   constexpr int LPS = D / 8, SPW = 64 / LPS, SPP = SPW * NWAVE, NPF = 4;
   const int ssl = lane / LPS, de = (lane % LPS) * 8;
-  const LayerPtrs& Lw = p.layers[l];
+  CLayerPtrs& Lw = ((CLayerPtrs*)p.layers)[l];
   const u32 arena_bytes = (u32)p.b * (u32)p.nkv * (u32)p.max_ctx * (u32)D * 2u;
   const __amdgpu_buffer_rsrc_t rk = rsrc(Lw.kc, arena_bytes);
   const __amdgpu_buffer_rsrc_t rv = rsrc(Lw.vc, arena_bytes);
   const u32 head_slot0 = ((u32)i * p.nkv + (u32)g) * (u32)p.max_ctx;
 
-  // Prefetch the first NPF passes of K/V (they do not depend on this step's q).
+  // Prefetch, before waiting for q: the first NPF passes of K/V, this lane's rotary row
+  // and the QK-norm gains (none of them depend on this step's activations).
   u32x4 kr[NPF], vr[NPF];
   auto issue = [&](int slot, int pass) {
     const int t = t0 + pass * SPP + wave * SPW + ssl;
@@ -537,50 +704,57 @@ __device__ bool op_attn(const Params& p, const int32_t* ins, float* smem, int ti
   };
 #pragma unroll
   for (int s = 0; s < NPF; ++s) issue(s, s);
+  const int half = D / 2;
+  const float* rt = p.rope + (size_t)st.pos[i] * half * 2;
+  float2 rot = make_float2(1.f, 0.f);
+  const int pe = tid % half;                  // rotary pair this thread applies
+  rot = *reinterpret_cast<const float2*>(rt + pe * 2);
+  float gq = 1.f, gk = 1.f;                   // QK-norm gains for dims lane and lane + 64
+  float gq2 = 1.f, gk2 = 1.f;
+  if (p.qk_norm) {
+    gq = __uint_as_float((u32)Lw.q_norm[lane] << 16);
+    gk = __uint_as_float((u32)Lw.k_norm[lane] << 16);
+    if (D > 64) {
+      gq2 = __uint_as_float((u32)Lw.q_norm[lane + 64] << 16);
+      gk2 = __uint_as_float((u32)Lw.k_norm[lane + 64] << 16);
+    }
+  }
 
   float* qs = smem;                 // [G][D]
   float* ks = qs + GT * D;          // [D]
   float* vs = ks + D;               // [D]
   float* wst = vs + D;              // [NWAVE][GT][D + 2]
-  float* misc = wst + NWAVE * GT * (D + 2);
 
-  // Wait for this group's q heads, k and v.
+  // Wait for this group's q heads, k and v (one batched round trip).
   const __amdgpu_buffer_rsrc_t ract = rsrc(p.act, p.act_bytes);
   const u32 base = p.off_qkv + (u32)l * p.st_qkv + (u32)i * (u32)((p.nh + 2 * p.nkv) * D);
-  float dummy = 0.f;
-  bool ok = wait_copy(p, ract, base + (u32)(g * G * D), G * D, qs, dummy, tid);
-  if (ok) ok = wait_copy(p, ract, base + (u32)(p.nh * D + g * D), D, ks, dummy, tid);
-  if (ok) ok = wait_copy(p, ract, base + (u32)((p.nh + p.nkv) * D + g * D), D, vs, dummy, tid);
+  bool ok = wait_copy3(p, st, ract, base + (u32)(g * G * D), G * D, qs, base + (u32)(p.nh * D + g * D), D, ks,
+                       base + (u32)((p.nh + p.nkv) * D + g * D), D, vs, tid);
   if (__syncthreads_or(!ok)) return false;
+  if (tl && tid == 0) tl[1] = clock_now();
 
   // Per-head RMSNorm on q and k (Qwen3-shaped models), then RoPE.
   if (p.qk_norm) {
     for (int hh = wave; hh <= G; hh += NWAVE) {
       float* v = (hh < G) ? qs + hh * D : ks;
-      const uint16_t* gn = (hh < G) ? Lw.q_norm : Lw.k_norm;
-      float ss = 0.f;
-      for (int e = lane; e < D; e += 64) ss += v[e] * v[e];
-      ss = wave_sum(ss);
+      float a0 = v[lane], a1 = (D > 64) ? v[lane + 64] : 0.f;
+      const float ss = wave_sum(a0 * a0 + a1 * a1);
       const float r = 1.0f / sqrtf(ss / (float)D + p.eps);
-      for (int e = lane; e < D; e += 64) v[e] = v[e] * r * __uint_as_float((u32)gn[e] << 16);
+      v[lane] = a0 * r * ((hh < G) ? gq : gk);
+      if (D > 64) v[lane + 64] = a1 * r * ((hh < G) ? gq2 : gk2);
     }
     __syncthreads();
   }
-  {
-    const int half = D / 2;
-    const float* rt = p.rope + (size_t)p.pos[i] * half * 2;
-    for (int u = tid; u < (G + 1) * half; u += NT) {
-      const int hh = u / half, e = u % half;
-      float* v = (hh < G) ? qs + hh * D : ks;
-      const float cs = rt[e * 2], sn = rt[e * 2 + 1];
-      const float a = v[e], b = v[e + half];
-      v[e] = a * cs - b * sn;
-      v[e + half] = b * cs + a * sn;
-    }
+  for (int u = tid; u < (G + 1) * half; u += NT) {
+    const int hh = u / half, e = u % half;     // e == pe since NT is a multiple of half
+    float* v = (hh < G) ? qs + hh * D : ks;
+    const float a = v[e], b = v[e + half];
+    v[e] = a * rot.x - b * rot.y;
+    v[e + half] = b * rot.x + a * rot.y;
   }
   __syncthreads();
-  if (p.taps) {
-    float* tb = p.taps + ((size_t)l * p.b + i) * p.tap_block;
+  if (st.taps) {
+    float* tb = st.taps + ((size_t)l * p.b + i) * p.tap_block;
     if (c == 0)
       for (int u = tid; u < G * D; u += NT) tb[p.tap_qrot + g * G * D + u] = qs[u];
     if (is_last)
@@ -614,18 +788,18 @@ __device__ bool op_attn(const Params& p, const int32_t* ins, float* smem, int ti
   auto update = [&](const float* kf, const float* vf, bool valid) {
 #pragma unroll
     for (int h = 0; h < GT; ++h) {
-      float s = 0.f;
+      float sc = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) s = fmaf(qr[h][e], kf[e], s);
+      for (int e = 0; e < 8; ++e) sc = fmaf(qr[h][e], kf[e], sc);
 #pragma unroll
-      for (int o = 1; o < LPS; o <<= 1) s += __shfl_xor(s, o, 64);
+      for (int o = 1; o < LPS; o <<= 1) sc += __shfl_xor(sc, o, 64);
       if (valid && h < G) {
-        const float mn = fmaxf(m[h], s);
+        const float mn = fmaxf(m[h], sc);
         const float a = (m[h] == -INFINITY) ? 0.f : exp2f(m[h] - mn);
-        const float pe = exp2f(s - mn);
-        ls[h] = ls[h] * a + pe;
+        const float pw = exp2f(sc - mn);
+        ls[h] = ls[h] * a + pw;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pe, vf[e], acc[h][e] * a);
+        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pw, vf[e], acc[h][e] * a);
         m[h] = mn;
       }
     }
@@ -678,55 +852,74 @@ __device__ bool op_attn(const Params& p, const int32_t* ins, float* smem, int ti
     }
   }
   __syncthreads();
-  // Merge the waves in order and publish this chunk's partial for each head.
+  // Merge the waves in order and publish this chunk's tagged partial for each head.
   const int nh = p.nh;
+  const int row = D + 2;
+  for (int u = tid; u < G * row; u += NT) {
+    const int h = u / row, e = u % row;
+    float M = -INFINITY;
+    for (int w = 0; w < NWAVE; ++w) M = fmaxf(M, wst[(w * GT + h) * row + D]);
+    float val;
+    if (e == D) {
+      val = M;
+    } else {
+      float A = 0.f;
+      for (int w = 0; w < NWAVE; ++w) {
+        const float* ws = wst + (w * GT + h) * row;
+        const float f = (ws[D] == -INFINITY) ? 0.f : exp2f(ws[D] - M);
+        A += ws[e] * f;           // e == D + 1 sums the softmax denominators
+      }
+      val = A;
+    }
+    u64* dst = p.part + ((((size_t)l * p.b + i) * nh + g * G + h) * p.maxc + c) * row;
+    st_tag(dst + e, val, st.epoch);
+  }
+  __syncthreads();   // LDS is reused by the next instruction
+  return true;
+}
+
+// Merge the split-KV partials of (lane i, KV head g) in chunk order and write the attention
+// output of its G query heads. The partials are staged in LDS as they arrive (tag polling).
+template <int D>
+__device__ __forceinline__ bool op_combine(CParams& p, const Step& st, const int32_t* ins, float* smem, int tid,
+                                           int lane, int wave, u64* tl) {
+  const int l = uni(ins[1]), gi = uni(ins[2]);
+  const int i = gi / p.nkv, g = gi % p.nkv;
+  const int G = p.G, nh = p.nh, row = D + 2;
+  const int nc = uni(chunks_of(p, st, i));
+  const __amdgpu_buffer_rsrc_t rpart = rsrc(p.part, (u32)((size_t)p.L * p.b * nh * p.maxc * row * 8));
+  const int per_head = nc * row;
+  const bool staged = G * per_head <= XSLAB_FLOATS;
+  float* cp = smem;                 // [G][nc][D + 2]
+  bool ok = true;
+  if (staged) {
+    // Heads of the group are contiguous: [G][maxc][row] words with the first nc chunks used.
+    for (int h = 0; h < G && ok; ++h) {
+      const u32 w0 = (u32)(((((size_t)l * p.b + i) * nh + g * G + h) * p.maxc) * row);
+      float dummy = 0.f;
+      ok = wait_copy(p, st, rpart, w0, per_head, cp + h * per_head, dummy, tid);
+    }
+  } else {
+    ok = false;   // capacity is checked at fm_create; never taken
+  }
+  if (__syncthreads_or(!ok)) return false;
+  if (tl && tid == 0) tl[1] = clock_now();
+  const u32 obase = p.off_o + (u32)l * p.st_o + (u32)i * (u32)(nh * D);
   for (int u = tid; u < G * D; u += NT) {
     const int h = u / D, e = u % D;
+    const float* src = cp + h * per_head;
     float M = -INFINITY;
-    for (int w = 0; w < NWAVE; ++w) M = fmaxf(M, wst[(w * GT + h) * (D + 2) + D]);
-    float Lsum = 0.f, A = 0.f;
-    for (int w = 0; w < NWAVE; ++w) {
-      const float* ws = wst + (w * GT + h) * (D + 2);
-      const float f = (ws[D] == -INFINITY) ? 0.f : exp2f(ws[D] - M);
-      Lsum += ws[D + 1] * f;
-      A += ws[e] * f;
+    for (int cc = 0; cc < nc; ++cc) M = fmaxf(M, src[cc * row + D]);
+    float den = 0.f, num = 0.f;
+    for (int cc = 0; cc < nc; ++cc) {
+      const float* pc = src + cc * row;
+      const float f = exp2f(pc[D] - M);
+      den += f * pc[D + 1];
+      num += f * pc[e];
     }
-    float* dst = p.part + (((size_t)i * nh + g * G + h) * p.maxc + c) * (D + 2);
-    st_dev(dst + e, A);
-    if (e == 0) { st_dev(dst + D, M); st_dev(dst + D + 1, Lsum); }
-  }
-  vm_wait0();
-  __syncthreads();
-  u32* arr = p.arrive + i * p.nkv + g;
-  int* flag = reinterpret_cast<int*>(misc);
-  if (tid == 0) {
-    const u32 old = __hip_atomic_fetch_add(arr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    flag[0] = (old == (u32)nc - 1u);
-    if (flag[0]) {
-      __hip_atomic_store(arr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      vm_wait0();
-    }
-  }
-  __syncthreads();
-  if (flag[0]) {
-    // Last arriver: log-sum-exp merge of the chunks in chunk order.
-    const u32 obase = p.off_o + (u32)l * p.st_o + (u32)i * (u32)(nh * D);
-    for (int u = tid; u < G * D; u += NT) {
-      const int h = u / D, e = u % D;
-      const float* src = p.part + ((size_t)i * nh + g * G + h) * p.maxc * (D + 2);
-      float M = -INFINITY;
-      for (int cc = 0; cc < nc; ++cc) M = fmaxf(M, ld_dev(src + cc * (D + 2) + D));
-      float den = 0.f, num = 0.f;
-      for (int cc = 0; cc < nc; ++cc) {
-        const float* pc = src + cc * (D + 2);
-        const float f = exp2f(ld_dev(pc + D) - M);
-        den += f * ld_dev(pc + D + 1);
-        num += f * ld_dev(pc + e);
-      }
-      const float o = num / den;
-      st_tag(p.act + obase + (u32)((g * G + h) * D + e), o, p.epoch);
-      if (p.taps) p.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_o + (g * G + h) * D + e] = o;
-    }
+    const float o = num / den;
+    st_tag(p.act + obase + (u32)((g * G + h) * D + e), o, st.epoch);
+    if (st.taps) st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_o + (g * G + h) * D + e] = o;
   }
   __syncthreads();
   return true;

@@ -47,7 +47,8 @@ class fm_plan_stats(ctypes.Structure):
 
 
 EXPORTS = ("fm_create", "fm_decode_step", "fm_decode_step_multilaunch", "fm_destroy", "fm_last_error",
-           "fm_set_taps", "fm_tap_count", "fm_plan_query", "fm_plan_export", "fm_status_string")
+           "fm_set_taps", "fm_tap_count", "fm_set_timeline", "fm_instruction_count", "fm_plan_query",
+           "fm_plan_export", "fm_status_string")
 
 _lib = None
 
@@ -68,6 +69,8 @@ def load():
     L.fm_destroy.argtypes = [P]
     L.fm_last_error.argtypes = [P, ctypes.POINTER(I32)]
     L.fm_set_taps.argtypes = [P, P]
+    L.fm_set_timeline.argtypes = [P, P]
+    L.fm_instruction_count.argtypes = [P]
     L.fm_tap_count.argtypes = [ctypes.POINTER(fm_model_cfg)]
     L.fm_tap_count.restype = ctypes.c_size_t
     L.fm_plan_query.argtypes = [ctypes.POINTER(fm_model_cfg), I32, ctypes.POINTER(fm_plan_stats)]
@@ -179,6 +182,14 @@ class Decoder:
     def set_taps(self, tap_buf):
         self._taps = tap_buf
         check(load().fm_set_taps(self.h, tap_buf.data_ptr() if tap_buf is not None else None), "fm_set_taps")
+
+    def set_timeline(self, buf):
+        """buf: CUDA int64 tensor of 8 * instruction_count() words, or None."""
+        self._tl = buf
+        check(load().fm_set_timeline(self.h, buf.data_ptr() if buf is not None else None), "fm_set_timeline")
+
+    def instruction_count(self) -> int:
+        return int(load().fm_instruction_count(self.h))
 
     def last_error(self) -> int:
         code = ctypes.c_int32(0)
