@@ -89,15 +89,15 @@ def main():
     cfg0 = get_config(args.config)
     total_steps = args.warmup + args.steps
     t_gen = time.time()
-    wl = make_workload(cfg0, steps=max(total_steps, cfg0["steps"]), threads=16)
+    # weights and KV prefill are drawn on the device (seeded, same distributions as the host recipe)
+    wl = make_workload(cfg0, steps=max(total_steps, cfg0["steps"]), device="cuda")
     cfg = wl.cfg
     gen_s = time.time() - t_gen
     b = cfg["batch"]
 
-    wdev = {k: v.cuda() for k, v in wl.weights.items() if k != "layers" and v is not None}
-    wdev["layers"] = [{k: v.cuda() for k, v in lw.items()} for lw in wl.weights["layers"]]
-    kc = [t.cuda() for t in wl.kcache]
-    vc = [t.cuda() for t in wl.vcache]
+    wdev = {k: v for k, v in wl.weights.items() if k != "layers" and v is not None}
+    wdev["layers"] = list(wl.weights["layers"])
+    kc, vc = list(wl.kcache), list(wl.vcache)
     dec = Decoder(cfg, wdev, kc, vc, n_workgroups=args.nwg, attn_items=args.attn_items)
 
     S = wl.S
@@ -206,11 +206,13 @@ def main():
     if not args.no_cpu:
         # CPU reference decoder on this host: a bounded sample of the same workload.
         from oracle.oracle import Oracle
-        wu = {k: as_u16(v) for k, v in wl.weights.items() if k != "layers" and v is not None}
-        wu["layers"] = [{k: as_u16(v) for k, v in lw.items()} for lw in wl.weights["layers"]]
+        wu = {k: as_u16(v.cpu()) for k, v in wl.weights.items() if k != "layers" and v is not None}
+        wu["layers"] = [{k: as_u16(v.cpu()) for k, v in lw.items()} for lw in wl.weights["layers"]]
         orc = Oracle(cfg, wu)
-        kco = [as_u16(t).copy() for t in wl.kcache]
-        vco = [as_u16(t).copy() for t in wl.vcache]
+        # the device arenas were advanced by the timed steps; the oracle starts from the prefill,
+        # which is untouched below each lane's context S_i
+        kco = [as_u16(t.cpu()).copy() for t in wl.kcache]
+        vco = [as_u16(t.cpu()).copy() for t in wl.vcache]
         threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
         tok = list(wl.start)
         n_cpu, t_cpu, span = 0, 0.0, cfg["max_ctx"] - max(S)

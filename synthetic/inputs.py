@@ -5,6 +5,11 @@ Weights: N(0, 0.02) drawn in fp32 by a per-tensor ``torch.Generator`` and rounde
 KV prefill: N(0, 1) bf16 in slots [0, S_i) of lane i; slots from S_i on hold zeros, or
 N(0, 100^2) noise when ``poison=True``. Start ids are uniform over the vocabulary; ragged
 contexts S_i are uniform integers over the workload's inclusive range.
+
+``device="cuda"`` draws weights and KV with torch's device generator instead (same
+distributions and per-tensor seeds, different streams of numbers): the full-size models
+take minutes to draw on the host and well under a second on the device. Either way both
+sides of a comparison get the very same tensors.
 """
 from __future__ import annotations
 
@@ -41,6 +46,15 @@ def _shapes(cfg: dict) -> list:
     return out
 
 
+def _draw_dev(seed: int, shape, kind: str, gains: str, device: str) -> torch.Tensor:
+    g = torch.Generator(device=device).manual_seed(seed)
+    if kind == "gain":
+        if gains == "ones":
+            return torch.ones(shape, dtype=torch.bfloat16, device=device)
+        return (torch.rand(shape, generator=g, device=device) + 0.5).to(torch.bfloat16)
+    return (torch.randn(shape, generator=g, device=device) * 0.02).to(torch.bfloat16)
+
+
 def _draw(seed: int, shape, kind: str, gains: str) -> torch.Tensor:
     g = torch.Generator().manual_seed(seed)
     if kind == "gain":
@@ -56,14 +70,19 @@ def _draw(seed: int, shape, kind: str, gains: str) -> torch.Tensor:
     return out.view(shape)
 
 
-def make_weights(cfg: dict, seed: int | None = None, gains: str = "ones", threads: int = 8) -> dict:
-    """All weights of one model as CPU bf16 tensors: {embed, final_norm, lm_head?, layers[l]{...}}."""
+def make_weights(cfg: dict, seed: int | None = None, gains: str = "ones", threads: int = 8,
+                 device: str = "cpu") -> dict:
+    """All weights of one model as bf16 tensors on ``device``:
+    {embed, final_norm, lm_head?, layers[l]{...}}."""
     if seed is None:
         seed = 1000 + cfg["k"]
     specs = _shapes(cfg)
     seeds = [(seed * 1_000_003 + idx * 7919) % (2**62) for idx in range(len(specs))]
-    with ThreadPoolExecutor(max_workers=threads) as ex:
-        tensors = list(ex.map(lambda a: _draw(a[1], a[0][2], a[0][3], gains), zip(specs, seeds)))
+    if device != "cpu":
+        tensors = [_draw_dev(sd, sp[2], sp[3], gains, device) for sp, sd in zip(specs, seeds)]
+    else:
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            tensors = list(ex.map(lambda a: _draw(a[1], a[0][2], a[0][3], gains), zip(specs, seeds)))
     w = {"layers": [dict() for _ in range(cfg["n_layers"])]}
     for (key, l, _, _), t in zip(specs, tensors):
         if l < 0:
@@ -84,27 +103,31 @@ def contexts(cfg: dict, seed: int | None = None) -> list:
 
 
 def make_kv(cfg: dict, S: list, max_ctx: int, seed: int | None = None, poison: bool = False,
-            threads: int = 8) -> tuple:
+            threads: int = 8, device: str = "cpu") -> tuple:
     """Per-layer K and V arenas [b][n_kv][max_ctx][d_h] bf16 with N(0,1) prefill in [0, S_i)."""
     if seed is None:
         seed = 2000 + cfg["k"]
     b, nkv, d, L = cfg["batch"], cfg["n_kv_heads"], cfg["head_dim"], cfg["n_layers"]
 
     def one(idx):
-        g = torch.Generator().manual_seed((seed * 1_000_003 + idx * 104729) % (2**62))
-        t = torch.zeros((b, nkv, max_ctx, d), dtype=torch.bfloat16)
+        g = torch.Generator(device=device).manual_seed((seed * 1_000_003 + idx * 104729) % (2**62))
+        t = torch.zeros((b, nkv, max_ctx, d), dtype=torch.bfloat16, device=device)
         for i in range(b):
-            t[i, :, : S[i], :] = torch.randn((nkv, S[i], d), generator=g).to(torch.bfloat16)
+            t[i, :, : S[i], :] = torch.randn((nkv, S[i], d), generator=g, device=device).to(torch.bfloat16)
         if poison:
             # a separate stream, so the prefill is identical with and without poison
-            gp = torch.Generator().manual_seed((seed * 1_000_003 + idx * 104729 + 1) % (2**62))
+            gp = torch.Generator(device=device).manual_seed((seed * 1_000_003 + idx * 104729 + 1) % (2**62))
             for i in range(b):
                 if S[i] < max_ctx:
-                    t[i, :, S[i]:, :] = (torch.randn((nkv, max_ctx - S[i], d), generator=gp) * 100.0).to(torch.bfloat16)
+                    t[i, :, S[i]:, :] = (torch.randn((nkv, max_ctx - S[i], d), generator=gp, device=device)
+                                         * 100.0).to(torch.bfloat16)
         return t
 
-    with ThreadPoolExecutor(max_workers=threads) as ex:
-        arenas = list(ex.map(one, range(2 * L)))
+    if device != "cpu":
+        arenas = [one(idx) for idx in range(2 * L)]
+    else:
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            arenas = list(ex.map(one, range(2 * L)))
     return arenas[0::2], arenas[1::2]
 
 
@@ -118,8 +141,8 @@ def make_start(cfg: dict, seed: int | None = None) -> list:
 @dataclass
 class Workload:
     cfg: dict            # shape + b + max_ctx
-    weights: dict        # CPU bf16 tensors
-    kcache: list         # per layer CPU bf16 [b][n_kv][max_ctx][d_h]
+    weights: dict        # bf16 tensors (on the device they were drawn on)
+    kcache: list         # per layer bf16 [b][n_kv][max_ctx][d_h]
     vcache: list
     S: list              # prefilled context per lane
     start: list          # start token per lane
@@ -127,12 +150,12 @@ class Workload:
 
 
 def make_workload(name_or_cfg, gains: str = "ones", poison: bool = False, steps: int | None = None,
-                  threads: int = 8) -> Workload:
+                  threads: int = 8, device: str = "cpu") -> Workload:
     from .configs import get_config
     cfg = get_config(name_or_cfg) if isinstance(name_or_cfg, str) else dict(name_or_cfg)
     steps = cfg["steps"] if steps is None else steps
     S = contexts(cfg)
     cfg["max_ctx"] = max(S) + steps
-    w = make_weights(cfg, gains=gains, threads=threads)
-    kc, vc = make_kv(cfg, S, cfg["max_ctx"], poison=poison, threads=threads)
+    w = make_weights(cfg, gains=gains, threads=threads, device=device)
+    kc, vc = make_kv(cfg, S, cfg["max_ctx"], poison=poison, threads=threads, device=device)
     return Workload(cfg=cfg, weights=w, kcache=kc, vcache=vc, S=S, start=make_start(cfg), steps=steps)
