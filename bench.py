@@ -81,7 +81,7 @@ def main():
     import numpy as np
     import torch
     from synthetic import get_config, make_workload, as_u16
-    from paper_2609_12379_amd.fm import Decoder, load
+    from paper_2609_12379_amd.fm import Decoder, load, plan_query
     from paper_2609_12379_amd.metrics import step_bytes
 
     load()  # fail loudly if the HIP library is missing
@@ -191,7 +191,7 @@ def main():
         ml = timed(args.steps, True) / args.steps
         out["ablation_multilaunch"] = {"ms_per_step": round(ml, 5), "us_per_token": round(ml * 1e3, 2),
                                        "mbu_pct": round(100 * sum(bytes_steps) / (ml * args.steps * 1e-3) / (PEAK_GBS * 1e9), 2),
-                                       "launches_per_step": 6 * cfg["n_layers"] + 1,
+                                       "launches_per_step": plan_query(cfg, 256).n_stages,
                                        "megakernel_speedup": round(ml / ms_per_step, 3)}
 
     if args.calib_copy_mb:

@@ -140,7 +140,7 @@ fm_status fm_decode_step(fm_handle *h, const int32_t *token_ids, const int32_t *
                          hipStream_t stream);
 
 /* The same step split into one kernel launch per operator stage: per layer a QKV,
- * attention, attention-combine, O-projection, gate/up and down launch, plus one LM-head launch. Each launch
+ * attention, O-projection, gate/up and down launch, plus one LM-head launch. Each launch
  * runs the same device code on the same per-CU queues. This is the ablation that the
  * single launch is measured against. Arguments and results are as for fm_decode_step.
  * The outputs are bit-identical to it. */
@@ -174,7 +174,9 @@ size_t fm_tap_count(const fm_model_cfg *cfg);
 /* Instruction timeline: when buf (device uint64, 8 * fm_instruction_count(h) words) is
  * non-NULL, each step records per queued instruction q, at buf[8q..8q+7], the device
  * wall-clock ticks {start, inputs ready, prologue done, stream done, end, workgroup, 0, 0}.
- * Marks an instruction does not have (attention items have no stream) are 0. The ticks are from the 100 MHz constant clock,
+ * For attention items the middle marks are: q/k/v ready, rotary and KV append done, partials
+ * published; the span from there to the end is the group merge (last item of a group only).
+ * Marks an instruction does not reach are 0. The ticks are from the 100 MHz constant clock,
  * read with s_memrealtime. These spans give the paper's busy fraction and tail spread
  * (Sec. 4.1, dependency gate). Pass NULL to turn the timeline off. */
 fm_status fm_set_timeline(fm_handle *h, uint64_t *buf);
@@ -187,8 +189,7 @@ int32_t fm_instruction_count(const fm_handle *h);
  *   instrs, and instrs holds int32[4] records {op, layer, a, b} (FM_OP_*).
  *   Its return codes: FM_ERR_CAPACITY when the arrays are shorter than fm_plan_query
  *   reports; FM_ERR_INVALID_ARG or FM_ERR_UNSUPPORTED for a bad cfg. */
-enum { FM_OP_QKV = 1, FM_OP_ATTN = 2, FM_OP_OPROJ = 3, FM_OP_GU = 4, FM_OP_DOWN = 5, FM_OP_LM = 6,
-       FM_OP_COMBINE = 7 };
+enum { FM_OP_QKV = 1, FM_OP_ATTN = 2, FM_OP_OPROJ = 3, FM_OP_GU = 4, FM_OP_DOWN = 5, FM_OP_LM = 6 };
 
 typedef struct fm_plan_stats {
   int32_t n_cu;              /* workgroups planned for */

@@ -8,8 +8,8 @@
 //     counter, so a handoff costs one store and one read round trip. There is no separate
 //     flag, no grid barrier, and no L2 writeback or invalidate (both cost microseconds on
 //     MI355X's eight non-coherent XCD L2s).
-//   * Attention partials are tagged words too; each (lane, KV head) has a combine
-//     instruction that waits for all of its chunks' partials.
+//   * Attention partials are tagged words too. Per (lane, KV head) an arrival count elects
+//     the group's last item, which waits for all of the group's partials and merges them.
 //   * Weights and the KV cache are streamed with non-temporal 128-bit buffer loads.
 #pragma once
 #include <hip/hip_runtime.h>
@@ -37,7 +37,7 @@ constexpr int NWAVE = NT / 64;
 #endif
 constexpr int NCTL = 0;
 constexpr int NSW = NWAVE - NCTL;
-constexpr int XSLAB_FLOATS = kSlabFloats;  // activation slab / combine staging (96 KB)
+constexpr int XSLAB_FLOATS = kSlabFloats;  // activation slab / partials staging (96 KB)
 constexpr int ROWACC_FLOATS = 8192;  // per-row dot products (and partials across slabs), 32 KB
 constexpr int RESID_FLOATS = 2048;   // residual rows staged for the epilogue (8 KB)
 constexpr int MISC_FLOATS = 1024;
@@ -72,6 +72,7 @@ struct Params {
   u32 st_x, st_qkv, st_o, st_x1, st_m;           // words per layer (all lanes)
   const uint16_t* zero_page;      // 64 KiB of zeros: the target of loads with nothing to load
   u64* part;                     // tagged [L][b][nh][maxc][d + 2]: split-KV partials
+  u32* attn_arrive;              // [L][b][nkv]: attention items published (reset by the last)
   u64* amax;                     // [b]
   u32* lm_arrive;                // [1]
   u32* abort_flag;               // [1]

@@ -54,8 +54,6 @@ __global__ __launch_bounds__(NT, 1) void step_kernel(const Params* __restrict__ 
     bool ok = true;
     if (op == FM_OP_ATTN) {
       ok = op_attn<D, GT>(P, st, ins, smem, tid, lane, wave, tl);
-    } else if (op == FM_OP_COMBINE) {
-      ok = op_combine<D>(P, st, ins, smem, tid, lane, wave, tl);
     } else if (op == FM_OP_GU) {
       ok = op_gemv<B, 2>(P, st, ins, smem, tid, lane, wave, tl);
     } else {

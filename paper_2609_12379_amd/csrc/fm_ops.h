@@ -50,26 +50,58 @@ __device__ __forceinline__ bool wait_pair(CParams& p, const Step& st, __amdgpu_b
 // Wait for n (even) tagged words at word offset w0 and copy their values to dst (LDS);
 // accumulates the sum of squares of the values this thread copied into ss. Each thread
 // issues up to WB pair loads before checking any of them, so a vector costs one round trip
-// when its producers are done; stale pairs are then re-polled one by one.
+// when its producers are done. Stale pairs are re-polled together, one round trip per
+// retry whatever their number. Values are consumed in index order once all are current, so
+// the sum of squares does not depend on which pairs had to wait.
 constexpr int WB = 8;
+template <int WBT>
+__device__ __forceinline__ bool repoll(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, const u32 (&w)[WBT],
+                                       u32x4 (&v)[WBT], u32 pend) {
+  const u64 t0 = clock_now();
+  int it = 0;
+  while (pend) {
+    __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+    for (int j = 0; j < WBT; ++j)
+      if (pend & (1u << j)) v[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, w[j] * 8u, 0, CPOL_SC1);
+#pragma unroll
+    for (int j = 0; j < WBT; ++j)
+      if ((pend & (1u << j)) && v[j].y == st.epoch && v[j].w == st.epoch) pend &= ~(1u << j);
+    if (pend && (++it & 63) == 0) {
+      if (clock_now() - t0 > WAIT_TICKS) {
+        raise_error(p, FM_DEV_WATCHDOG);
+        return false;
+      }
+      if (abort_raised(p)) return false;
+    }
+  }
+  return true;
+}
+
 template <int WBT = WB>
 __device__ __forceinline__ bool wait_copy_t(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, u32 w0, int n,
                                             float* dst, float& ss, int t, int nthr) {
   for (int k0 = t * 2; k0 < n; k0 += nthr * 2 * WBT) {
     u32x4 v[WBT];
+    u32 w[WBT];
+    u32 pend = 0;
 #pragma unroll
     for (int j = 0; j < WBT; ++j) {
       const int k = k0 + j * nthr * 2;
-      v[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, (k < n) ? (w0 + (u32)k) * 8u : 0xFFFFFFF0u, 0, CPOL_SC1);
+      w[j] = (k < n) ? w0 + (u32)k : 0x1FFFFFFEu;
+      v[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, (k < n) ? w[j] * 8u : 0xFFFFFFF0u, 0, CPOL_SC1);
     }
 #pragma unroll
     for (int j = 0; j < WBT; ++j) {
       const int k = k0 + j * nthr * 2;
+      if (k < n && (v[j].y != st.epoch || v[j].w != st.epoch)) pend |= 1u << j;
+    }
+    if (pend && !repoll<WBT>(p, st, ra, w, v, pend)) return false;
+#pragma unroll
+    for (int j = 0; j < WBT; ++j) {
+      const int k = k0 + j * nthr * 2;
       if (k < n) {
-        float a = __uint_as_float(v[j].x), b = __uint_as_float(v[j].z);
-        if (v[j].y != st.epoch || v[j].w != st.epoch) {
-          if (!wait_pair(p, st, ra, w0 + (u32)k, a, b)) return false;
-        }
+        const float a = __uint_as_float(v[j].x), b = __uint_as_float(v[j].z);
         ss += a * a + b * b;
         if (dst) {
           dst[k] = a;
@@ -86,41 +118,53 @@ __device__ __forceinline__ bool wait_copy(CParams& p, const Step& st, __amdgpu_b
   return wait_copy_t<WB>(p, st, ra, w0, n, dst, ss, tid, NT);
 }
 
+// Waits for n (even) tagged words whose pair k (k even) lives at word where(k) and goes to
+// LDS at dst(k): the same batched polling as wait_copy_t over an arbitrary index map.
+template <int WBT, class Where>
+__device__ __forceinline__ bool wait_copy_map(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, int n,
+                                              Where where, int tid) {
+  for (int k0 = tid * 2; k0 < n; k0 += NT * 2 * WBT) {
+    u32x4 v[WBT];
+    u32 w[WBT];
+    u32 pend = 0;
+#pragma unroll
+    for (int j = 0; j < WBT; ++j) {
+      const int k = k0 + j * NT * 2;
+      float* d = nullptr;
+      w[j] = 0x1FFFFFFEu;
+      if (k < n) where(k, w[j], d);
+      v[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, (k < n) ? w[j] * 8u : 0xFFFFFFF0u, 0, CPOL_SC1);
+    }
+#pragma unroll
+    for (int j = 0; j < WBT; ++j) {
+      const int k = k0 + j * NT * 2;
+      if (k < n && (v[j].y != st.epoch || v[j].w != st.epoch)) pend |= 1u << j;
+    }
+    if (pend && !repoll<WBT>(p, st, ra, w, v, pend)) return false;
+#pragma unroll
+    for (int j = 0; j < WBT; ++j) {
+      const int k = k0 + j * NT * 2;
+      if (k < n) {
+        u32 ww; float* d;
+        where(k, ww, d);
+        d[0] = __uint_as_float(v[j].x);
+        d[1] = __uint_as_float(v[j].z);
+      }
+    }
+  }
+  return true;
+}
+
 // Like wait_copy for three word ranges at once (one round trip when all are ready).
 __device__ __forceinline__ bool wait_copy3(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra,
                                            u32 wa, int na, float* da, u32 wb, int nb, float* db,
                                            u32 wc, int nc, float* dc, int tid) {
-  const int n = na + nb + nc;
   auto where = [&](int k, u32& w, float*& d) {
     if (k < na) { w = wa + (u32)k; d = da + k; }
     else if (k < na + nb) { w = wb + (u32)(k - na); d = db + (k - na); }
     else { w = wc + (u32)(k - na - nb); d = dc + (k - na - nb); }
   };
-  for (int k0 = tid * 2; k0 < n; k0 += NT * 2 * WB) {
-    u32x4 v[WB];
-#pragma unroll
-    for (int j = 0; j < WB; ++j) {
-      const int k = k0 + j * NT * 2;
-      u32 w = 0; float* d = nullptr;
-      if (k < n) where(k, w, d);
-      v[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, (k < n) ? w * 8u : 0xFFFFFFF0u, 0, CPOL_SC1);
-    }
-#pragma unroll
-    for (int j = 0; j < WB; ++j) {
-      const int k = k0 + j * NT * 2;
-      if (k < n) {
-        u32 w; float* d;
-        where(k, w, d);
-        float a = __uint_as_float(v[j].x), b = __uint_as_float(v[j].z);
-        if (v[j].y != st.epoch || v[j].w != st.epoch) {
-          if (!wait_pair(p, st, ra, w, a, b)) return false;
-        }
-        d[0] = a;
-        d[1] = b;
-      }
-    }
-  }
-  return true;
+  return wait_copy_map<WB>(p, st, ra, na + nb + nc, where, tid);
 }
 
 // Sum over the workgroup; every thread gets the total. Uses misc[0..NWAVE).
@@ -629,8 +673,8 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
 // group's raw q (G heads), k and v, applies QK-norm and RoPE; the item holding the last chunk
 // also rounds the new k/v to bf16 and appends them at slot kv_len. It then runs an online
 // softmax over its slots (base-2 exponent, log2(e)/sqrt(d) folded into q) and publishes one
-// tagged partial (max, sum, weighted V) per head. A separate combine instruction per
-// (lane, KV head) waits for the partials and merges them in chunk order (log-sum-exp).
+// tagged partial (max, sum, weighted V) per head. The last of a (lane, KV head) group's items
+// to finish merges the group's partials in chunk order (log-sum-exp) and writes its output.
 
 __device__ __forceinline__ bool item_map(CParams& p, const Step& st, int j, int& i, int& g, int& c, int& nc,
                                          int& t0, int& t1) {
@@ -804,6 +848,7 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
       }
     }
   };
+  if (tl && tid == 0) tl[2] = clock_now();
   const int n_arena = t_end - t0;
   const int npass = n_arena > 0 ? (n_arena + SPP - 1) / SPP : 0;
   for (int pb = 0; pb < npass; pb += NPF) {
@@ -874,36 +919,45 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
     u64* dst = p.part + ((((size_t)l * p.b + i) * nh + g * G + h) * p.maxc + c) * row;
     st_tag(dst + e, val, st.epoch);
   }
+  // The group's last item to publish merges all of its partials. The arrival count only
+  // elects that item: the partials themselves are read by tag, so the count needs no
+  // ordering against them. The elected item resets the count for the next step.
+  int* flag = reinterpret_cast<int*>(smem + XSLAB_FLOATS + ROWACC_FLOATS + RESID_FLOATS);
+  if (tid == 0) {
+    u32* arrive = p.attn_arrive + ((size_t)l * p.b + i) * p.nkv + g;
+    const u32 old = __hip_atomic_fetch_add(arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int last = old == (u32)(nc - 1) ? 1 : 0;
+    if (last) __hip_atomic_store(arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *flag = last;
+  }
+  __syncthreads();
+  if (tl && tid == 0) tl[3] = clock_now();
+  const bool last = uni(*flag) != 0;
+  if (last && !combine_group<D>(p, st, l, i, g, nc, smem, tid)) return false;
   __syncthreads();   // LDS is reused by the next instruction
   return true;
 }
 
-// Merge the split-KV partials of (lane i, KV head g) in chunk order and write the attention
-// output of its G query heads. The partials are staged in LDS as they arrive (tag polling).
+// Merge the split-KV partials of (lane i, KV head g) in chunk order (log-sum-exp) and write
+// the attention output of its G query heads. All nc partials are staged in LDS first, one
+// batched round trip when they are all published.
 template <int D>
-__device__ __forceinline__ bool op_combine(CParams& p, const Step& st, const int32_t* ins, float* smem, int tid,
-                                           int lane, int wave, u64* tl) {
-  const int l = uni(ins[1]), gi = uni(ins[2]);
-  const int i = gi / p.nkv, g = gi % p.nkv;
+__device__ __forceinline__ bool combine_group(CParams& p, const Step& st, int l, int i, int g, int nc, float* smem,
+                                              int tid) {
   const int G = p.G, nh = p.nh, row = D + 2;
-  const int nc = uni(chunks_of(p, st, i));
   const __amdgpu_buffer_rsrc_t rpart = rsrc(p.part, (u32)((size_t)p.L * p.b * nh * p.maxc * row * 8));
-  const int per_head = nc * row;
-  const bool staged = G * per_head <= XSLAB_FLOATS;
-  float* cp = smem;                 // [G][nc][D + 2]
-  bool ok = true;
-  if (staged) {
-    // Heads of the group are contiguous: [G][maxc][row] words with the first nc chunks used.
-    for (int h = 0; h < G && ok; ++h) {
-      const u32 w0 = (u32)(((((size_t)l * p.b + i) * nh + g * G + h) * p.maxc) * row);
-      float dummy = 0.f;
-      ok = wait_copy(p, st, rpart, w0, per_head, cp + h * per_head, dummy, tid);
-    }
-  } else {
-    ok = false;   // capacity is checked at fm_create; never taken
-  }
+  const int per_head = nc * row;          // even: row is even
+  float* cp = smem;                       // [G][nc][D + 2]
+  // The group's heads are contiguous: [G][maxc][row] words, the first nc chunks in use.
+  const u32 w0 = (u32)((((size_t)l * p.b + i) * nh + (size_t)g * G) * p.maxc * row);
+  const u32 hstride = (u32)(p.maxc * row);
+  auto where = [&](int k, u32& w, float*& d) {
+    const int h = k / per_head, r = k - h * per_head;
+    w = w0 + (u32)h * hstride + (u32)r;
+    d = cp + k;
+  };
+  const bool ok = wait_copy_map<WB>(p, st, rpart, G * per_head, where, tid);
   if (__syncthreads_or(!ok)) return false;
-  if (tl && tid == 0) tl[1] = clock_now();
   const u32 obase = p.off_o + (u32)l * p.st_o + (u32)i * (u32)(nh * D);
   for (int u = tid; u < G * D; u += NT) {
     const int h = u / D, e = u % D;

@@ -53,7 +53,7 @@ fm_status build_plan(const fm_model_cfg& c, int32_t nwg, Plan& p, std::string* w
   // Attention work items per layer. Each (lane, KV head) needs at least one item, and the
   // per-step chunking (see the kernel's item map) needs P > n_kv * b.
   // Automatic count: about one item per workgroup (more when there are many (lane, KV head)
-  // groups), capped so that one group's chunk partials fit the combine's LDS staging.
+  // groups), capped so that one group's chunk partials fit the merge's LDS staging.
   int32_t P = c.attn_items;
   if (P == 0) {
     int32_t need = nkv * b;
@@ -71,7 +71,7 @@ fm_status build_plan(const fm_model_cfg& c, int32_t nwg, Plan& p, std::string* w
   p.nwg = nwg;
   p.attn_items = P;
   p.attn_max_chunks = (P - nkv * b) / nkv + 1;
-  p.n_stages = 6 * L + 1;
+  p.n_stages = 5 * L + 1;
 
   std::vector<std::vector<Instr>> q(nwg);
   std::vector<double> bytes(nwg, 0.0);
@@ -88,9 +88,6 @@ fm_status build_plan(const fm_model_cfg& c, int32_t nwg, Plan& p, std::string* w
   for (int32_t l = 0; l < L; ++l) {
     gemv(FM_OP_QKV, l, qkv_rows, h, 1);
     for (int32_t j = 0; j < P; ++j) q[j % nwg].push_back(Instr{FM_OP_ATTN, l, j, 0});
-    // One combine per (lane, KV head), dealt from the far end of the workgroup range so the
-    // combines mostly land on workgroups other than those holding the group's first chunks.
-    for (int32_t gi = 0; gi < b * nkv; ++gi) q[nwg - 1 - (gi % nwg)].push_back(Instr{FM_OP_COMBINE, l, gi, 0});
     gemv(FM_OP_OPROJ, l, h, (int64_t)nh * d, 1);
     gemv(FM_OP_GU, l, inter, h, 2);
     gemv(FM_OP_DOWN, l, h, inter, 1);
@@ -122,7 +119,7 @@ fm_status build_plan(const fm_model_cfg& c, int32_t nwg, Plan& p, std::string* w
   fm_plan_stats& s = p.stats;
   s.n_cu = nwg;
   s.n_instr = (int32_t)p.instrs.size();
-  s.n_types = 7;
+  s.n_types = 6;
   int32_t min_pl = 1 << 30;
   for (int32_t l = 0; l < L; ++l) {
     int32_t cnt = 0;
@@ -130,9 +127,9 @@ fm_status build_plan(const fm_model_cfg& c, int32_t nwg, Plan& p, std::string* w
     min_pl = std::min(min_pl, cnt);
   }
   s.min_instr_per_layer = min_pl;
-  // Per layer: tagged qkv, o, x1, m and x vectors (5) plus one tagged partial block per
-  // (lane, KV head); per step: the LM arrival counter and b argmax words.
-  s.n_counters = 5 * L + L * nkv * b + 1 + b;
+  // Per layer: tagged qkv, o, x1, m and x vectors (5), plus one tagged partial block and one
+  // arrival counter per (lane, KV head); per step: the LM arrival counter and b argmax words.
+  s.n_counters = 5 * L + 2 * L * nkv * b + 1 + b;
   s.attn_items = P;
   s.attn_max_chunks = p.attn_max_chunks;
   s.n_stages = p.n_stages;

@@ -16,8 +16,8 @@ namespace fm {
 
 // One instruction: op (FM_OP_*), layer, and an operand range whose meaning depends on op:
 //   GEMV ops  -> output rows [a, b) of that op's matrix (QKV rows index [W_q; W_k; W_v]),
-//   FM_OP_ATTN -> attention work item a of the layer (mapped to lane/KV head/slots per step),
-//   FM_OP_COMBINE -> merge of the split-KV partials of (lane a / n_kv, KV head a % n_kv).
+//   FM_OP_ATTN -> attention work item a of the layer (mapped to lane/KV head/slots per step;
+//                 the last item of each (lane, KV head) group also merges the group's partials).
 struct Instr {
   int32_t op, layer, a, b;
 };
@@ -27,7 +27,7 @@ struct Plan {
   int32_t attn_items = 0;      // P: items per layer
   int32_t attn_max_chunks = 0; // partials capacity per (lane, KV head)
   int32_t n_lm_instr = 0;      // workgroups holding LM-head rows
-  int32_t n_stages = 0;        // 6 per layer + LM head
+  int32_t n_stages = 0;        // 5 per layer + LM head
   std::vector<Instr> instrs;
   std::vector<int32_t> qoff;       // [nwg + 1]
   std::vector<int32_t> stage_rng;  // [n_stages][nwg][2]: each queue's sub-range per stage
@@ -38,12 +38,12 @@ struct Plan {
 fm_status build_plan(const fm_model_cfg& cfg, int32_t nwg, Plan& plan, std::string* why);
 
 // Stage index of an instruction in the multi-launch order.
-// Per layer: QKV, attention items, combine, O projection, gate/up, down; then the LM head.
+// Per layer: QKV, attention items, O projection, gate/up, down; then the LM head.
 inline int32_t stage_of(const Instr& in, int32_t n_layers) {
-  if (in.op == FM_OP_LM) return 6 * n_layers;
-  const int32_t order = in.op == FM_OP_QKV ? 0 : in.op == FM_OP_ATTN ? 1 : in.op == FM_OP_COMBINE ? 2
-                      : in.op == FM_OP_OPROJ ? 3 : in.op == FM_OP_GU ? 4 : 5;
-  return 6 * in.layer + order;
+  if (in.op == FM_OP_LM) return 5 * n_layers;
+  const int32_t order = in.op == FM_OP_QKV ? 0 : in.op == FM_OP_ATTN ? 1 : in.op == FM_OP_OPROJ ? 2
+                      : in.op == FM_OP_GU ? 3 : 4;
+  return 5 * in.layer + order;
 }
 
 }  // namespace fm

@@ -3,8 +3,8 @@
 * the library loads and exports every function that include/fm.h declares;
 * argument validation of the host-checkable errors (Sec. 4.1's compiler rejects what the
   kernel cannot run);
-* the schedule compiler's queues: every output row, attention item and combine appears
-  exactly once per layer, each queue is in one global topological order, and the structural
+* the schedule compiler's queues: every output row and attention item appears exactly once
+  per layer, each queue is in one global topological order, and the structural
   gates of Sec. 4.3 (instruction types, instructions per layer, queue imbalance, counters)
   hold on every full-size shape;
 * deadlock freedom: a simulation of all queues that lets a workgroup run its next
@@ -25,8 +25,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "fm.h")
 
 FULL = ["qwen3-0.6b", "llama3.2-1b", "llama2-7b", "qwen3-8b", "llama2-13b", "qwen3-8b-b1", "llama2-13b-b1"]
-OP_QKV, OP_ATTN, OP_OPROJ, OP_GU, OP_DOWN, OP_LM, OP_COMBINE = 1, 2, 3, 4, 5, 6, 7
-STAGE = {OP_QKV: 0, OP_ATTN: 1, OP_COMBINE: 2, OP_OPROJ: 3, OP_GU: 4, OP_DOWN: 5}
+OP_QKV, OP_ATTN, OP_OPROJ, OP_GU, OP_DOWN, OP_LM = 1, 2, 3, 4, 5, 6
+STAGE = {OP_QKV: 0, OP_ATTN: 1, OP_OPROJ: 2, OP_GU: 3, OP_DOWN: 4}
 
 
 @pytest.fixture(scope="module")
@@ -168,15 +168,12 @@ def check_plan(cfg, nwg, fm):
         elif op == OP_ATTN:
             assert 0 <= a < P and 0 <= layer < L
             cover.setdefault((op, layer), []).append((int(a), int(a) + 1))
-        elif op == OP_COMBINE:
-            assert 0 <= a < b * nkv and 0 <= layer < L
-            cover.setdefault((op, layer), []).append((int(a), int(a) + 1))
         else:
             raise AssertionError(f"unknown op {op}")
     # every row / item / group exactly once
     for l in range(L):
         for op, n in ((OP_QKV, rows[OP_QKV]), (OP_OPROJ, rows[OP_OPROJ]), (OP_GU, rows[OP_GU]),
-                      (OP_DOWN, rows[OP_DOWN]), (OP_ATTN, P), (OP_COMBINE, b * nkv)):
+                      (OP_DOWN, rows[OP_DOWN]), (OP_ATTN, P)):
             iv = sorted(cover[(op, l)])
             assert iv[0][0] == 0 and iv[-1][1] == n and all(x[1] == y[0] for x, y in zip(iv, iv[1:])), (op, l)
     iv = sorted(cover[(OP_LM, L)])
@@ -189,7 +186,7 @@ def check_plan(cfg, nwg, fm):
     assert s.n_types >= 5
     assert s.min_instr_per_layer >= 6
     assert s.n_counters >= 4 * L
-    assert s.n_stages == 6 * L + 1
+    assert s.n_stages == 5 * L + 1
     # imbalance in weight bytes per queue, recomputed from the exported queues
     cols = _gemv_cols(cfg)
     per = np.zeros(nwg)
@@ -218,14 +215,15 @@ def test_plan_small_shapes(fm, name, nwg):
 
 def simulate(cfg, qoff, ins, P):
     """Run all queues with coarse dependencies (a superset of what the kernel waits on):
-    QKV(l) needs all of DOWN(l-1); ATTN(l) all of QKV(l); COMBINE(l) all of ATTN(l); OPROJ(l)
-    all of COMBINE(l); GU(l) all of OPROJ(l); DOWN(l) all of GU(l); LM all of DOWN(L-1).
+    QKV(l) needs all of DOWN(l-1); ATTN(l) all of QKV(l); OPROJ(l) all of ATTN(l) (the merge
+    runs inside the group's last item); GU(l) all of OPROJ(l); DOWN(l) all of GU(l); LM all of
+    DOWN(L-1).
     Returns True when every queue drains."""
     L = cfg["n_layers"]
     total, done = {}, {}
     for o, l, _, _ in ins:
         total[(int(o), int(l))] = total.get((int(o), int(l)), 0) + 1
-    prev = {OP_ATTN: OP_QKV, OP_COMBINE: OP_ATTN, OP_OPROJ: OP_COMBINE, OP_GU: OP_OPROJ, OP_DOWN: OP_GU}
+    prev = {OP_ATTN: OP_QKV, OP_OPROJ: OP_ATTN, OP_GU: OP_OPROJ, OP_DOWN: OP_GU}
 
     def ready(o, l):
         if o == OP_QKV:
