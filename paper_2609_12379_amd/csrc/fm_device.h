@@ -8,8 +8,8 @@
 //     counter, so a handoff costs one store and one read round trip. There is no separate
 //     flag, no grid barrier, and no L2 writeback or invalidate (both cost microseconds on
 //     MI355X's eight non-coherent XCD L2s).
-//   * Attention partials are tagged words too. Per (lane, KV head) an arrival count elects
-//     the group's last item, which waits for all of the group's partials and merges them.
+//   * Attention partials are tagged words too. The item holding a (lane, KV head) group's
+//     last chunk waits for the group's other partials and merges them.
 //   * Weights and the KV cache are streamed with non-temporal 128-bit buffer loads.
 #pragma once
 #include <hip/hip_runtime.h>
@@ -35,7 +35,10 @@ constexpr int NWAVE = NT / 64;
 #ifndef FM_RING
 #define FM_RING 16
 #endif
-constexpr int NCTL = 0;
+#ifndef FM_NCTL
+#define FM_NCTL 0
+#endif
+constexpr int NCTL = FM_NCTL;
 constexpr int NSW = NWAVE - NCTL;
 constexpr int XSLAB_FLOATS = kSlabFloats;  // activation slab / partials staging (96 KB)
 constexpr int ROWACC_FLOATS = 8192;  // per-row dot products (and partials across slabs), 32 KB
@@ -72,7 +75,6 @@ struct Params {
   u32 st_x, st_qkv, st_o, st_x1, st_m;           // words per layer (all lanes)
   const uint16_t* zero_page;      // 64 KiB of zeros: the target of loads with nothing to load
   u64* part;                     // tagged [L][b][nh][maxc][d + 2]: split-KV partials
-  u32* attn_arrive;              // [L][b][nkv]: attention items published (reset by the last)
   u64* amax;                     // [b]
   u32* lm_arrive;                // [1]
   u32* abort_flag;               // [1]
@@ -133,12 +135,6 @@ __device__ __forceinline__ u64 tag(float v, u32 epoch) { return ((u64)epoch << 3
 __device__ __forceinline__ void st_tag(u64* p, float v, u32 epoch) {
   __hip_atomic_store(p, tag(v, epoch), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void st_dev(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float ld_dev(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -153,41 +149,6 @@ __device__ __forceinline__ float row16_sum(float s) {
   s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x141, 0xF, 0xF, false));  // half-row mirror
   s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x140, 0xF, 0xF, false));  // row mirror
   return s;
-}
-
-// Transpose-reduce of four per-lane partial sums a0..a3 over the 64 lanes of a wave.
-// Returns, in every lane of 16-lane row R, the full sum of a_{map(R)} with
-// map = {0, 2, 1, 3}: lanes 0-15 hold sum(a0), 16-31 sum(a2), 32-47 sum(a1), 48-63 sum(a3).
-// gfx950's v_permlane32_swap / v_permlane16_swap exchange half-waves / half-rows in the VALU.
-__device__ __forceinline__ float reduce4(float a0, float a1, float a2, float a3) {
-  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(a0), __float_as_uint(a1), false, false);
-  const float s01 = __uint_as_float(p[0]) + __uint_as_float(p[1]);
-  auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(a2), __float_as_uint(a3), false, false);
-  const float s23 = __uint_as_float(q[0]) + __uint_as_float(q[1]);
-  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(s01), __float_as_uint(s23), false, false);
-  return row16_sum(__uint_as_float(r[0]) + __uint_as_float(r[1]));
-}
-
-// Same for two rows: lanes 0-31 hold sum(a0), lanes 32-63 sum(a1).
-__device__ __forceinline__ float reduce2(float a0, float a1) {
-  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(a0), __float_as_uint(a1), false, false);
-  const float s = __uint_as_float(p[0]) + __uint_as_float(p[1]);
-  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(s), __float_as_uint(s), false, false);
-  return row16_sum(__uint_as_float(r[0]) + __uint_as_float(r[1]));
-}
-
-// Full 64-lane sum in every lane.
-__device__ __forceinline__ float reduce1(float a) {
-  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(a), false, false);
-  const float s = __uint_as_float(p[0]) + __uint_as_float(p[1]);
-  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(s), __float_as_uint(s), false, false);
-  return row16_sum(__uint_as_float(r[0]) + __uint_as_float(r[1]));
-}
-
-// Value of lane (l xor 32).
-__device__ __forceinline__ float swap_halves(float v) {
-  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(p[1]);
 }
 
 __device__ __forceinline__ u64 clock_now() { return wall_clock64(); }

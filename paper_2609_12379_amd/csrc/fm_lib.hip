@@ -32,7 +32,6 @@ struct fm_handle {
   int32_t *d_instrs = nullptr, *d_qoff = nullptr, *d_stage = nullptr;
   u64* d_act = nullptr;
   u64* d_part = nullptr;
-  u32* d_arrive = nullptr;
   u64* d_amax = nullptr;
   u32* d_lm_arrive = nullptr;
   u32* d_abort = nullptr;
@@ -58,7 +57,7 @@ int round_batch(int b) { return b <= 1 ? 1 : b <= 2 ? 2 : b <= 4 ? 4 : 8; }
 void free_handle(fm_handle* h) {
   if (!h) return;
   hipFree(h->d_layers); hipFree(h->d_rope); hipFree(h->d_instrs); hipFree(h->d_qoff);
-  hipFree(h->d_stage); hipFree(h->d_act); hipFree(h->d_part); hipFree(h->d_arrive);
+  hipFree(h->d_stage); hipFree(h->d_act); hipFree(h->d_part);
   hipFree(h->d_amax); hipFree(h->d_lm_arrive); hipFree(h->d_abort); hipFree(h->d_params); hipFree(h->d_zero);
   if (h->h_err) hipHostFree(h->h_err);
   delete h;
@@ -252,8 +251,6 @@ fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_k
   if (part_words * 8 >= (1ull << 32)) { free_handle(h); return FM_ERR_CAPACITY; }
   HIP_TRY(hipMalloc(&h->d_part, part_words * 8));
   HIP_TRY(hipMemset(h->d_part, 0, part_words * 8));
-  HIP_TRY(hipMalloc(&h->d_arrive, L * b * nkv * 4));
-  HIP_TRY(hipMemset(h->d_arrive, 0, L * b * nkv * 4));
   HIP_TRY(hipMalloc(&h->d_amax, b * 8));
   HIP_TRY(hipMemset(h->d_amax, 0, b * 8));
   HIP_TRY(hipMalloc(&h->d_lm_arrive, 64));
@@ -288,7 +285,7 @@ fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_k
   p.off_x1 = p.off_o + (u32)L * p.st_o;
   p.off_m = p.off_x1 + (u32)L * p.st_x1;
   p.zero_page = h->d_zero;
-  p.part = h->d_part; p.attn_arrive = h->d_arrive; p.amax = h->d_amax; p.lm_arrive = h->d_lm_arrive;
+  p.part = h->d_part; p.amax = h->d_amax; p.lm_arrive = h->d_lm_arrive;
   p.abort_flag = h->d_abort; p.err_host = h->d_err;
   const TapOff t = tap_offsets(c);
   p.tap_block = t.block;

@@ -1,6 +1,6 @@
 // Operator bodies executed by the step interpreter: GEMV row-tiles (with fused RMSNorm
 // prologue, residual/SiLU/argmax epilogues) and split-KV attention work items (with fused
-// QK-norm, RoPE, KV append, online softmax and a last-arriver log-sum-exp combine).
+// QK-norm, RoPE, KV append, online softmax and the log-sum-exp merge of a group's chunks).
 #pragma once
 #include <type_traits>
 
@@ -54,6 +54,8 @@ __device__ __forceinline__ bool wait_pair(CParams& p, const Step& st, __amdgpu_b
 // retry whatever their number. Values are consumed in index order once all are current, so
 // the sum of squares does not depend on which pairs had to wait.
 constexpr int WB = 8;
+// Pair loads in flight per thread when only the control waves stage a GEMV input.
+constexpr int WBC = NCTL ? 16 : WB;
 template <int WBT>
 __device__ __forceinline__ bool repoll(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, const u32 (&w)[WBT],
                                        u32x4 (&v)[WBT], u32 pend) {
@@ -399,7 +401,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
           dst[k] = a; dst[k + 1] = b;
         }
       } else {
-        if (!wait_copy_t<WB>(p, st, ract, in_w + (u32)i * in_stride + (u32)k0, kn, dst, ss, ct, nct)) return false;
+        if (!wait_copy_t<WBC>(p, st, ract, in_w + (u32)i * in_stride + (u32)k0, kn, dst, ss, ct, nct)) return false;
       }
       if (accumulate_ss) {
 #pragma unroll
@@ -462,7 +464,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
           ss += a * a + b * b;
         }
       } else {
-        ok = wait_copy_t<WB>(p, st, ract, in_w + (u32)i * in_stride, K, nullptr, ss, ct, nct);
+        ok = wait_copy_t<WBC>(p, st, ract, in_w + (u32)i * in_stride, K, nullptr, ss, ct, nct);
       }
       ssv[i] += ss;
     }
@@ -668,21 +670,30 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
 //
 // Per layer the step has P work items. At run time item j maps, from kv_lens alone, to a
 // lane i, a KV head g and a chunk [t0, t1) of that lane's slots 0..kv_len: every
-// (lane, KV head) gets ceil((kv_len+1)/T) chunks of at most T slots, with T chosen so the
-// total chunk count fits in P (ragged lanes are thus balanced per step). An item reads its
-// group's raw q (G heads), k and v, applies QK-norm and RoPE; the item holding the last chunk
-// also rounds the new k/v to bf16 and appends them at slot kv_len. It then runs an online
-// softmax over its slots (base-2 exponent, log2(e)/sqrt(d) folded into q) and publishes one
-// tagged partial (max, sum, weighted V) per head. The last of a (lane, KV head) group's items
-// to finish merges the group's partials in chunk order (log-sum-exp) and writes its output.
+// (lane, KV head) gets ceil((kv_len+1)/T) chunks of at most T slots. T is the smallest
+// multiple of an item's pass width (the slots all waves cover at once) for which the chunks
+// fit in P, so ragged lanes are balanced per step and no pass runs mostly empty.
+// An item reads its group's raw q (G heads), k and v and applies QK-norm and RoPE. The item
+// holding the group's last chunk also rounds the new k/v to bf16 and appends them at slot
+// kv_len. Each item runs an online softmax over its slots (Eq. 1; base-2 exponent with
+// log2(e)/sqrt(d) folded into q) and yields one partial (max, sum, weighted V) per head.
+// The last chunk's item is the group's merger: the others publish their partials as tagged
+// words, and the merger combines them with its own in chunk order (log-sum-exp) and writes
+// the group's attention output.
 
-__device__ __forceinline__ bool item_map(CParams& p, const Step& st, int j, int& i, int& g, int& c, int& nc,
-                                         int& t0, int& t1) {
+// Chunk length of this step (see above); spp is the pass width.
+__device__ __forceinline__ int chunk_len(CParams& p, const Step& st, int spp) {
   long long total = 0;
   for (int ii = 0; ii < p.b; ++ii) total += st.kvl[ii] + 1;
   total *= p.nkv;
   const long long denom = p.P - p.nkv * p.b;
-  const int T = (int)((total + denom - 1) / denom);
+  const int T0 = (int)((total + denom - 1) / denom);
+  return ((T0 + spp - 1) / spp) * spp;
+}
+
+__device__ __forceinline__ bool item_map(CParams& p, const Step& st, int j, int spp, int& i, int& g, int& c,
+                                         int& nc, int& t0, int& t1) {
+  const int T = chunk_len(p, st, spp);
   int idx = j;
   for (int ii = 0; ii < p.b; ++ii) {
     const int W = st.kvl[ii] + 1;
@@ -698,16 +709,6 @@ __device__ __forceinline__ bool item_map(CParams& p, const Step& st, int j, int&
   return false;
 }
 
-// Chunk count of (lane i, any KV head) under the same map.
-__device__ __forceinline__ int chunks_of(CParams& p, const Step& st, int i) {
-  long long total = 0;
-  for (int ii = 0; ii < p.b; ++ii) total += st.kvl[ii] + 1;
-  total *= p.nkv;
-  const long long denom = p.P - p.nkv * p.b;
-  const int T = (int)((total + denom - 1) / denom);
-  return (st.kvl[i] + 1 + T - 1) / T;
-}
-
 __device__ __forceinline__ void sm_merge(float& m, float& l, float* acc, float mo, float lo, const float* acco) {
   const float mn = fmaxf(m, mo);
   const float a = (m == -INFINITY) ? 0.f : exp2f(m - mn);
@@ -718,18 +719,104 @@ __device__ __forceinline__ void sm_merge(float& m, float& l, float* acc, float m
   m = mn;
 }
 
+// Sum within each 8-lane half-row; every lane of it gets the total (DPP).
+__device__ __forceinline__ float row8_sum(float s) {
+  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0xB1, 0xF, 0xF, false));   // quad [1,0,3,2]
+  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x4E, 0xF, 0xF, false));   // quad [2,3,0,1]
+  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x141, 0xF, 0xF, false));  // half-row mirror
+  return s;
+}
+
+// Value of lane (lane xor 8), (lane xor 16), (lane xor 32), in the VALU.
+__device__ __forceinline__ float lane_xor8(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xF, 0xF, false));  // row rotate 8
+}
+__device__ __forceinline__ float lane_xor16(float v, int lane) {
+  // permlane16_swap(a, a): the first result holds row r & ~1 in both rows of a pair, the
+  // second row r | 1.
+  auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(((lane >> 4) & 1) ? p[0] : p[1]);
+}
+__device__ __forceinline__ float lane_xor32(float v, int lane) {
+  // permlane32_swap(a, a): the first result holds lanes 0-31 in both halves, the second 32-63.
+  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float((lane >> 5) ? p[0] : p[1]);
+}
+template <int O>
+__device__ __forceinline__ float lane_xor(float v, int lane) {
+  static_assert(O == 8 || O == 16 || O == 32, "exchange distance");
+  return O == 8 ? lane_xor8(v) : (O == 16 ? lane_xor16(v, lane) : lane_xor32(v, lane));
+}
+
+// Merges the partials of the slot groups of a wave that share this lane's dims: lanes
+// (lane xor O) for O = LPS, 2 LPS, ..., 32.
+template <int O, int GT>
+__device__ __forceinline__ void merge_slot_groups(float (&m)[GT], float (&ls)[GT], float (&acc)[GT][8], int lane) {
+  if constexpr (O <= 32) {
+#pragma unroll
+    for (int h = 0; h < GT; ++h) {
+      const float mo = lane_xor<O>(m[h], lane), lo = lane_xor<O>(ls[h], lane);
+      float ao[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ao[e] = lane_xor<O>(acc[h][e], lane);
+      sm_merge(m[h], ls[h], acc[h], mo, lo, ao);
+    }
+    merge_slot_groups<O * 2, GT>(m, ls, acc, lane);
+  }
+}
+
+// The merger of (lane i, KV head g): waits for the tagged partials of chunks 0..nc-2 of each
+// of the group's heads (staged into cp next to its own chunk nc-1, already in LDS), combines
+// them in chunk order (log-sum-exp) and writes the attention output of the G query heads.
+template <int D>
+__device__ __forceinline__ bool merge_group(CParams& p, const Step& st, int l, int i, int g, int nc, float* cp,
+                                            int tid) {
+  const int G = p.G, nh = p.nh, row = D + 2;
+  const __amdgpu_buffer_rsrc_t rpart = rsrc(p.part, (u32)((size_t)p.L * p.b * nh * p.maxc * row * 8));
+  const int per_head = nc * row;
+  const int others = (nc - 1) * row;      // even: row is even
+  // The group's heads are contiguous: [G][maxc][row] words, the first nc chunks in use.
+  const u32 w0 = (u32)((((size_t)l * p.b + i) * nh + (size_t)g * G) * p.maxc * row);
+  const u32 hstride = (u32)(p.maxc * row);
+  auto where = [&](int k, u32& w, float*& d) {
+    const int h = k / others, r = k - h * others;
+    w = w0 + (u32)h * hstride + (u32)r;
+    d = cp + h * per_head + r;
+  };
+  const bool ok = wait_copy_map<WB>(p, st, rpart, G * others, where, tid);
+  if (__syncthreads_or(!ok)) return false;
+  const u32 obase = p.off_o + (u32)l * p.st_o + (u32)i * (u32)(nh * D);
+  for (int u = tid; u < G * D; u += NT) {
+    const int h = u / D, e = u % D;
+    const float* src = cp + h * per_head;
+    float M = -INFINITY;
+    for (int cc = 0; cc < nc; ++cc) M = fmaxf(M, src[cc * row + D]);
+    float den = 0.f, num = 0.f;
+    for (int cc = 0; cc < nc; ++cc) {
+      const float* pc = src + cc * row;
+      const float f = exp2f(pc[D] - M);
+      den += f * pc[D + 1];
+      num += f * pc[e];
+    }
+    const float o = num / den;
+    st_tag(p.act + obase + (u32)((g * G + h) * D + e), o, st.epoch);
+    if (st.taps) st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_o + (g * G + h) * D + e] = o;
+  }
+  return true;
+}
+
 template <int D, int GT>
 __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_t* ins, float* smem, int tid,
                                         int lane, int wave, u64* tl) {
+  constexpr int LPS = D / 8, SPW = 64 / LPS, SPP = SPW * NWAVE, NPF = 4;
   const int l = uni(ins[1]), j = uni(ins[2]);
   int i, g, c, nc, t0, t1;
-  if (!item_map(p, st, j, i, g, c, nc, t0, t1)) return true;
-  i = uni(i); g = uni(g); c = uni(c); t0 = uni(t0); t1 = uni(t1);
+  if (!item_map(p, st, j, SPP, i, g, c, nc, t0, t1)) return true;
+  i = uni(i); g = uni(g); c = uni(c); nc = uni(nc); t0 = uni(t0); t1 = uni(t1);
   const int G = p.G;
   const int kvl = uni(st.kvl[i]);
-  const bool is_last = (t1 == kvl + 1);
+  const bool is_last = (t1 == kvl + 1);     // holds the new slot; merges the group
   const int t_end = min(t1, kvl);            // slots [t0, t_end) come from the arena
-  constexpr int LPS = D / 8, SPW = 64 / LPS, SPP = SPW * NWAVE, NPF = 4;
   const int ssl = lane / LPS, de = (lane % LPS) * 8;
   CLayerPtrs& Lw = ((CLayerPtrs*)p.layers)[l];
   const u32 arena_bytes = (u32)p.b * (u32)p.nkv * (u32)p.max_ctx * (u32)D * 2u;
@@ -764,7 +851,11 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
     }
   }
 
-  float* qs = smem;                 // [G][D]
+  // LDS: the slab region holds the merger's partials [G][nc][D + 2]; this item's working
+  // vectors live in the row-sum and residual regions behind it.
+  static_assert(GT * D + 2 * D + NWAVE * GT * (D + 2) <= ROWACC_FLOATS + RESID_FLOATS, "attention LDS");
+  float* cp = smem;
+  float* qs = smem + XSLAB_FLOATS;  // [G][D]
   float* ks = qs + GT * D;          // [D]
   float* vs = ks + D;               // [D]
   float* wst = vs + D;              // [NWAVE][GT][D + 2]
@@ -814,8 +905,8 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
       ks[e] = __uint_as_float((u32)kb << 16);
       vs[e] = __uint_as_float((u32)vb << 16);
     }
+    __syncthreads();
   }
-  __syncthreads();
 
   float qr[GT][8];
 #pragma unroll
@@ -835,8 +926,7 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
       float sc = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) sc = fmaf(qr[h][e], kf[e], sc);
-#pragma unroll
-      for (int o = 1; o < LPS; o <<= 1) sc += __shfl_xor(sc, o, 64);
+      sc = (LPS == 16) ? row16_sum(sc) : row8_sum(sc);
       if (valid && h < G) {
         const float mn = fmaxf(m[h], sc);
         const float a = (m[h] == -INFINITY) ? 0.f : exp2f(m[h] - mn);
@@ -873,18 +963,7 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
     for (int e = 0; e < 8; ++e) { kf[e] = ks[de + e]; vf[e] = vs[de + e]; }
     update(kf, vf, ssl == 0);
   }
-  // Merge the slot groups of the wave (lanes with equal dims, different slots).
-#pragma unroll
-  for (int o = LPS; o < 64; o <<= 1) {
-#pragma unroll
-    for (int h = 0; h < GT; ++h) {
-      const float mo = __shfl_xor(m[h], o, 64), lo = __shfl_xor(ls[h], o, 64);
-      float ao[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) ao[e] = __shfl_xor(acc[h][e], o, 64);
-      sm_merge(m[h], ls[h], acc[h], mo, lo, ao);
-    }
-  }
+  merge_slot_groups<LPS, GT>(m, ls, acc, lane);
   if (ssl == 0) {
 #pragma unroll
     for (int h = 0; h < GT; ++h) {
@@ -897,7 +976,8 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
     }
   }
   __syncthreads();
-  // Merge the waves in order and publish this chunk's tagged partial for each head.
+  // Merge the waves in order: the chunk's partial for each head. The merger keeps its own in
+  // LDS (slot nc - 1 of cp); the other items publish theirs as tagged words.
   const int nh = p.nh;
   const int row = D + 2;
   for (int u = tid; u < G * row; u += NT) {
@@ -916,66 +996,16 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
       }
       val = A;
     }
-    u64* dst = p.part + ((((size_t)l * p.b + i) * nh + g * G + h) * p.maxc + c) * row;
-    st_tag(dst + e, val, st.epoch);
-  }
-  // The group's last item to publish merges all of its partials. The arrival count only
-  // elects that item: the partials themselves are read by tag, so the count needs no
-  // ordering against them. The elected item resets the count for the next step.
-  int* flag = reinterpret_cast<int*>(smem + XSLAB_FLOATS + ROWACC_FLOATS + RESID_FLOATS);
-  if (tid == 0) {
-    u32* arrive = p.attn_arrive + ((size_t)l * p.b + i) * p.nkv + g;
-    const u32 old = __hip_atomic_fetch_add(arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int last = old == (u32)(nc - 1) ? 1 : 0;
-    if (last) __hip_atomic_store(arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    *flag = last;
-  }
-  __syncthreads();
-  if (tl && tid == 0) tl[3] = clock_now();
-  const bool last = uni(*flag) != 0;
-  if (last && !combine_group<D>(p, st, l, i, g, nc, smem, tid)) return false;
-  __syncthreads();   // LDS is reused by the next instruction
-  return true;
-}
-
-// Merge the split-KV partials of (lane i, KV head g) in chunk order (log-sum-exp) and write
-// the attention output of its G query heads. All nc partials are staged in LDS first, one
-// batched round trip when they are all published.
-template <int D>
-__device__ __forceinline__ bool combine_group(CParams& p, const Step& st, int l, int i, int g, int nc, float* smem,
-                                              int tid) {
-  const int G = p.G, nh = p.nh, row = D + 2;
-  const __amdgpu_buffer_rsrc_t rpart = rsrc(p.part, (u32)((size_t)p.L * p.b * nh * p.maxc * row * 8));
-  const int per_head = nc * row;          // even: row is even
-  float* cp = smem;                       // [G][nc][D + 2]
-  // The group's heads are contiguous: [G][maxc][row] words, the first nc chunks in use.
-  const u32 w0 = (u32)((((size_t)l * p.b + i) * nh + (size_t)g * G) * p.maxc * row);
-  const u32 hstride = (u32)(p.maxc * row);
-  auto where = [&](int k, u32& w, float*& d) {
-    const int h = k / per_head, r = k - h * per_head;
-    w = w0 + (u32)h * hstride + (u32)r;
-    d = cp + k;
-  };
-  const bool ok = wait_copy_map<WB>(p, st, rpart, G * per_head, where, tid);
-  if (__syncthreads_or(!ok)) return false;
-  const u32 obase = p.off_o + (u32)l * p.st_o + (u32)i * (u32)(nh * D);
-  for (int u = tid; u < G * D; u += NT) {
-    const int h = u / D, e = u % D;
-    const float* src = cp + h * per_head;
-    float M = -INFINITY;
-    for (int cc = 0; cc < nc; ++cc) M = fmaxf(M, src[cc * row + D]);
-    float den = 0.f, num = 0.f;
-    for (int cc = 0; cc < nc; ++cc) {
-      const float* pc = src + cc * row;
-      const float f = exp2f(pc[D] - M);
-      den += f * pc[D + 1];
-      num += f * pc[e];
+    if (is_last) {
+      cp[(h * nc + (nc - 1)) * row + e] = val;
+    } else {
+      u64* dst = p.part + ((((size_t)l * p.b + i) * nh + g * G + h) * p.maxc + c) * row;
+      st_tag(dst + e, val, st.epoch);
     }
-    const float o = num / den;
-    st_tag(p.act + obase + (u32)((g * G + h) * D + e), o, st.epoch);
-    if (st.taps) st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_o + (g * G + h) * D + e] = o;
   }
-  __syncthreads();
+  if (tl && tid == 0) tl[3] = clock_now();
+  if (is_last && !merge_group<D>(p, st, l, i, g, nc, cp, tid)) return false;
+  __syncthreads();   // LDS is reused by the next instruction
   return true;
 }
 

@@ -127,9 +127,9 @@ fm_status build_plan(const fm_model_cfg& c, int32_t nwg, Plan& p, std::string* w
     min_pl = std::min(min_pl, cnt);
   }
   s.min_instr_per_layer = min_pl;
-  // Per layer: tagged qkv, o, x1, m and x vectors (5), plus one tagged partial block and one
-  // arrival counter per (lane, KV head); per step: the LM arrival counter and b argmax words.
-  s.n_counters = 5 * L + 2 * L * nkv * b + 1 + b;
+  // Per layer: tagged qkv, o, x1, m and x vectors (5) plus one tagged partial block per
+  // (lane, KV head); per step: the LM arrival counter and b argmax words.
+  s.n_counters = 5 * L + L * nkv * b + 1 + b;
   s.attn_items = P;
   s.attn_max_chunks = p.attn_max_chunks;
   s.n_stages = p.n_stages;
