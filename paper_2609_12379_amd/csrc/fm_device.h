@@ -23,6 +23,8 @@ namespace dev {
 typedef uint32_t u32;
 typedef uint64_t u64;
 typedef u32 u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int NT = 512;              // threads per workgroup
 constexpr int NWAVE = NT / 64;
@@ -33,18 +35,26 @@ constexpr int NWAVE = NT / 64;
 // Measured on MI355X: splitting roles (2 control + 6 streaming waves) was slower than
 // letting all 8 waves do both, so NCTL = 0 (every wave streams and stages).
 #ifndef FM_RING
-#define FM_RING 16
+#define FM_RING 4
 #endif
 #ifndef FM_NCTL
 #define FM_NCTL 0
 #endif
 constexpr int NCTL = FM_NCTL;
 constexpr int NSW = NWAVE - NCTL;
-constexpr int XSLAB_FLOATS = kSlabFloats;  // activation slab / partials staging (96 KB)
-constexpr int ROWACC_FLOATS = 8192;  // per-row dot products (and partials across slabs), 32 KB
-constexpr int RESID_FLOATS = 2048;   // residual rows staged for the epilogue (8 KB)
-constexpr int MISC_FLOATS = 1024;
-constexpr int LDS_FLOATS = XSLAB_FLOATS + ROWACC_FLOATS + RESID_FLOATS + MISC_FLOATS;
+// LDS of a workgroup (158 KB of the CU's 160 KB), laid out per operator:
+//   GEMV tiles: [activation slab][row sums ROWACC][residual rows RESID][MISC];
+//   attention items: [merger's partials, kMergeFloats] ... [item scratch ATT][MISC].
+// Matrix-core (batched) tiles need fewer row sums and a larger slab.
+constexpr int LDS_FLOATS = 40448;
+constexpr int MISC_FLOATS = 1024;   // block reductions, argmax keys
+constexpr int RESID_FLOATS = 2048;  // residual rows staged for the epilogue
+constexpr int ATT_FLOATS = 9600;    // q heads, k, v and per-wave partials of one item (G <= 8, d <= 128)
+template <int B> constexpr int rowacc_floats() { return B >= 4 ? 4096 : 8192; }
+template <int B> constexpr int xslab_floats() {
+  return LDS_FLOATS - MISC_FLOATS - RESID_FLOATS - rowacc_floats<B>();
+}
+static_assert(kMergeFloats + ATT_FLOATS + MISC_FLOATS <= LDS_FLOATS, "attention LDS layout");
 
 constexpr u32 CPOL_NT = 2;    // non-temporal (streaming)
 constexpr u32 CPOL_SC1 = 16;  // device-scope coherent

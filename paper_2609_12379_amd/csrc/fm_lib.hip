@@ -199,20 +199,23 @@ fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_k
     // Per-tile LDS needs: residual rows, and per-row partials when K spans several slabs.
     auto rows_max = [&](int64_t n) { return (n + nwg - 1) / nwg; };
     if (rows_max(hd) * Bt > RESID_FLOATS) { free_handle(h); return FM_ERR_CAPACITY; }
-    // rowacc holds [KP][rows][nw][B]; KP > 1 only when the tile has fewer than NWAVE quads.
+    const int64_t rowacc_cap = Bt >= 4 ? rowacc_floats<4>() : rowacc_floats<1>();
+    // rowacc holds [KP][rows][nw][B]; KP > 1 only when the tile has fewer than NWAVE row
+    // groups (4 weight rows per group, 16 on the matrix-core path of batched steps).
+    const int64_t grp = Bt >= 4 ? 16 : 4;
     auto needs = [&](int64_t rows, int nw) {
-      const int64_t r = rows_max(rows), quads = (r * nw + 3) / 4;
+      const int64_t r = rows_max(rows), quads = (r * nw + grp - 1) / grp;
       const int64_t kp = quads < NWAVE ? NWAVE / std::max<int64_t>(quads, 1) : 1;
       return r * nw * Bt * kp;
     };
-    if (needs(nqkv, 1) > ROWACC_FLOATS || needs(hd, 1) > ROWACC_FLOATS || needs(inter, 2) > ROWACC_FLOATS ||
-        needs(V, 1) > ROWACC_FLOATS) {
+    if (needs(nqkv, 1) > rowacc_cap || needs(hd, 1) > rowacc_cap || needs(inter, 2) > rowacc_cap ||
+        needs(V, 1) > rowacc_cap) {
       free_handle(h);
       return FM_ERR_CAPACITY;
     }
   }
   // The group merge stages one group's partials in LDS: G heads x chunks x (d + 2) floats.
-  if ((nh / nkv) * (int64_t)P.attn_max_chunks * (d + 2) > XSLAB_FLOATS) { free_handle(h); return FM_ERR_CAPACITY; }
+  if ((nh / nkv) * (int64_t)P.attn_max_chunks * (d + 2) > kMergeFloats) { free_handle(h); return FM_ERR_CAPACITY; }
   h->kernel = kernel_for(Bt, (int)d, (int)(nh / nkv));
   if (!h->kernel) { free_handle(h); return FM_ERR_UNSUPPORTED; }
   int occ = 0;

@@ -2,7 +2,6 @@
 #pragma once
 
 namespace fm {
-// LDS floats a workgroup has for one operator's staged data: the activation slab of a GEMV
-// tile, or the split-KV partials of one (lane, KV head) group in the combine.
-constexpr int kSlabFloats = 24576;
+// LDS floats for the split-KV partials of one (lane, KV head) group, staged by its merger.
+constexpr int kMergeFloats = 24576;
 }  // namespace fm

@@ -80,18 +80,22 @@ __device__ __forceinline__ bool repoll(CParams& p, const Step& st, __amdgpu_buff
   return true;
 }
 
-template <int WBT = WB>
-__device__ __forceinline__ bool wait_copy_t(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, u32 w0, int n,
-                                            float* dst, float& ss, int t, int nthr) {
+// Polls n (even) tagged words from word w0 on, pairs k = t*2 + j*nthr*2 as wait_copy_t does,
+// and hands each pair, once current, to use(k, a, b, side) in index order. side is the u32
+// at side[k / 2] (a pair of bf16 gains), loaded with the poll; 0 when side is null.
+template <int WBT, class Use>
+__device__ __forceinline__ bool wait_pairs(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, u32 w0, int n,
+                                           const u32* side, Use use, int t, int nthr) {
   for (int k0 = t * 2; k0 < n; k0 += nthr * 2 * WBT) {
     u32x4 v[WBT];
-    u32 w[WBT];
+    u32 w[WBT], sv[WBT];
     u32 pend = 0;
 #pragma unroll
     for (int j = 0; j < WBT; ++j) {
       const int k = k0 + j * nthr * 2;
       w[j] = (k < n) ? w0 + (u32)k : 0x1FFFFFFEu;
       v[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, (k < n) ? w[j] * 8u : 0xFFFFFFF0u, 0, CPOL_SC1);
+      sv[j] = (side && k < n) ? side[k >> 1] : 0u;
     }
 #pragma unroll
     for (int j = 0; j < WBT; ++j) {
@@ -102,17 +106,23 @@ __device__ __forceinline__ bool wait_copy_t(CParams& p, const Step& st, __amdgpu
 #pragma unroll
     for (int j = 0; j < WBT; ++j) {
       const int k = k0 + j * nthr * 2;
-      if (k < n) {
-        const float a = __uint_as_float(v[j].x), b = __uint_as_float(v[j].z);
-        ss += a * a + b * b;
-        if (dst) {
-          dst[k] = a;
-          dst[k + 1] = b;
-        }
-      }
+      if (k < n) use(k, __uint_as_float(v[j].x), __uint_as_float(v[j].z), sv[j]);
     }
   }
   return true;
+}
+
+template <int WBT = WB>
+__device__ __forceinline__ bool wait_copy_t(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, u32 w0, int n,
+                                            float* dst, float& ss, int t, int nthr) {
+  auto use = [&](int k, float a, float b, u32) {
+    ss += a * a + b * b;
+    if (dst) {
+      dst[k] = a;
+      dst[k + 1] = b;
+    }
+  };
+  return wait_pairs<WBT>(p, st, ra, w0, n, nullptr, use, t, nthr);
 }
 
 __device__ __forceinline__ bool wait_copy(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, u32 w0, int n,
@@ -203,6 +213,14 @@ __device__ __forceinline__ u32 ordered(float f) {
 //
 // Every ring slot issues exactly one global load (so the compiler counts loads in flight
 // exactly); lanes with nothing to load read a zeroed page instead.
+//
+// Batched tiles (B >= 4) run the products on the matrix cores instead (a skinny GEMM):
+// a unit is then 16 weight rows x 32 columns, loaded in the A-operand layout of
+// v_mfma_f32_16x16x32_bf16 (lane l: row l % 16, columns 8 (l / 16) .. + 8, still one 16 B
+// load per lane). The B operand is the activation slab: each fp32 value x is split into
+// bf16 hi = rne(x) and lo = rne(x - hi), and both halves go through the matrix core into
+// the same fp32 accumulator, so the product keeps about 16 bits of the activation's
+// mantissa. Lanes 16 .. of the B operand's 16 columns (batch lanes past B) are zero.
 
 struct GemvGeom {
   int K, Ks, nslab;           // columns, slab width, slabs
@@ -235,20 +253,27 @@ __device__ __forceinline__ void cursor_next(GemvCursor& c, const GemvGeom& g, in
   if (c.sg == g.SP) cursor_at(c, g, c.it + 1, wave);
 }
 
-// Issues the load of the cursor's unit into `dst`. Units that do not exist (past the wave's
-// items, or past the slab's segments in a short last K part) issue nothing: a load whose
-// result is never used would still have to complete before its registers are reused.
-// Lanes of an existing unit that fall outside the matrix (rows past the tile, the ragged
-// last segment) read their zero-page slot instead.
-template <int NW>
+// Issues the load of the cursor's unit into `dst`: exactly one load per call, so the number
+// of loads in flight behind any ring slot is a compile-time constant and the wait for a slot
+// is a partial one (vmcnt(U - 1)). Lanes with nothing to load (units past the wave's items
+// or the slab's segments, rows past the tile, the ragged last segment) read their slot of
+// the zero page, which stays in cache.
+// Unit shape: 4 rows x 128 columns (VALU tiles) or 16 rows x 32 columns (matrix-core tiles).
+template <bool MF> struct UnitShape {
+  static constexpr int rows = MF ? 16 : 4, cols = MF ? 32 : 128;
+  __device__ static int row(int lane) { return MF ? (lane & 15) : (lane >> 4); }
+  __device__ static int col8(int lane) { return MF ? (lane >> 4) : (lane & 15); }
+};
+
+template <int NW, bool MF>
 __device__ __forceinline__ void load_unit(u32x4& dst, const GemvGeom& g, const GemvCursor& c, int lane, int op,
                                           int ra, const uint16_t* m0, const uint16_t* m1, const uint16_t* m2,
                                           int n0, int n1, const uint16_t* zero_page) {
+  using US = UnitShape<MF>;
   const int seg = c.pt * g.SP + c.sg;
-  if (!(c.live && seg < g.nseg)) return;
-  const int wr = c.qd * 4 + (lane >> 4);
-  const int k = g.k0 + seg * 128 + (lane & 15) * 8;
-  const bool valid = wr < g.nwr && k < g.kend;
+  const int wr = c.qd * US::rows + US::row(lane);
+  const int k = g.k0 + seg * US::cols + US::col8(lane) * 8;
+  const bool valid = c.live && seg < g.nseg && wr < g.nwr && k < g.kend;
   const uint16_t* ptr;
   if (NW == 2) {
     ptr = ((wr & 1) ? m1 : m0) + (size_t)(ra + (wr >> 1)) * g.K + k;
@@ -317,38 +342,47 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
   // Geometry (all wave-uniform).
   GemvGeom g;
   g.K = K;
+  constexpr bool MF = (B >= 4);           // matrix-core tiles for batched steps
+  using US = UnitShape<MF>;
+  constexpr int XSF = xslab_floats<B>();
   {
     const int Kpad = (K + 127) & ~127;
-    int ks = (XSLAB_FLOATS / B) & ~127;
+    // fp32 slab [B][Ks], or three bf16 planes [3][B][Ks] (6 bytes per value) on the matrix cores
+    const int ks = (MF ? (XSF * 4) / (6 * B) : XSF / B) & ~127;
     g.Ks = ks < Kpad ? ks : Kpad;
   }
   g.K = uni(K);
   g.Ks = uni(g.Ks);
   g.nslab = uni((K + g.Ks - 1) / g.Ks);
   g.nwr = uni(nr * NW);
-  g.NQ = uni((g.nwr + 3) >> 2);
+  g.NQ = uni((g.nwr + US::rows - 1) / US::rows);
   auto set_slab = [&](int s) {
     g.k0 = uni(s * g.Ks);
     const int kn = min(g.Ks, K - g.k0);
     g.kend = uni(g.k0 + kn);
-    g.nseg = uni((kn + 127) >> 7);
-    int kp = 1;
-    if (g.nslab == 1 && g.NQ < NSW) {
-      kp = NSW / g.NQ;
-      if (kp > g.nseg) kp = g.nseg;
+    g.nseg = uni((kn + US::cols - 1) / US::cols);
+    if (s == 0) {
+      // K parts are fixed for the whole tile (every slab splits its columns the same way,
+      // so each (row group, part) item stays with one wave and its row sums add up across
+      // slabs); a shorter last slab just leaves some parts empty.
+      int kp = 1;
+      if (g.NQ < NSW) {
+        kp = NSW / g.NQ;
+        if (kp > g.nseg) kp = g.nseg;
+      }
+      g.KP = uni(kp);
+      g.nitems = uni(g.NQ * g.KP);
+      g.items_w = uni((wave < NSW && g.nitems > wave) ? (g.nitems - wave + NSW - 1) / NSW : 0);
     }
-    g.KP = uni(kp);
     g.SP = uni((g.nseg + g.KP - 1) / g.KP);
-    g.nitems = uni(g.NQ * g.KP);
-    g.items_w = uni((wave < NSW && g.nitems > wave) ? (g.nitems - wave + NSW - 1) / NSW : 0);
   };
   set_slab(0);
   const int KP0 = g.KP;
 
   float* xs = smem;
-  float* rowacc = smem + XSLAB_FLOATS;   // [KP][nr][NW][B]
-  float* resid = rowacc + ROWACC_FLOATS;
-  float* misc = resid + RESID_FLOATS;
+  float* rowacc = smem + XSF;            // [KP][nr][NW][B]
+  float* resid = rowacc + rowacc_floats<B>();
+  float* misc = smem + LDS_FLOATS - MISC_FLOATS;
 
   // 1. Prefetch the first U units (and the RMSNorm gains), before waiting for the input.
   const uint16_t* zp = zero_slot(p, wave, lane);
@@ -358,20 +392,23 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
   cursor_at(ci, g, 0, wave);
 #pragma unroll
   for (int sl = 0; sl < U; ++sl) {
-    load_unit<NW>(ring[sl], g, ci, lane, op, ra, m0, m1, m2, nq, nk, zp);
+    load_unit<NW, MF>(ring[sl], g, ci, lane, op, ra, m0, m1, m2, nq, nk, zp);
     cursor_next(ci, g, wave);
   }
 
   constexpr int GP = 8;                  // gain pairs held in registers (K <= 8192)
   u32 gpair[GP];
-  const bool gains_in_regs = gain && g.nslab == 1 && K <= GP * NT * 2;
+  const bool gains_in_regs = !MF && gain && g.nslab == 1 && K <= GP * NT * 2;
 #pragma unroll
   for (int jj = 0; jj < GP; ++jj) {
     const int k = tid * 2 + jj * NT * 2;
     gpair[jj] = (gains_in_regs && k < K) ? *reinterpret_cast<const u32*>(gain + k) : 0u;
   }
 
-  // 2. Input: wait for the producers, then stage (normalised) values in LDS.
+  // 2. Input: wait for the producers, then stage the values in LDS. VALU tiles hold the
+  //    normalised fp32 values. Matrix-core tiles hold x * g split into three bf16 planes
+  //    (hi + mid + lo = x * g to about 2^-24 relative); their 1/rms is applied to the
+  //    finished rows in the epilogue, since a slab sees only part of x.
   bool ok = true;
   float rs[B];
 #pragma unroll
@@ -379,6 +416,57 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
   // Inputs are polled and staged by the control waves (ct = thread index among them).
   const bool ctl = (NCTL == 0) || wave >= NSW;
   const int ct = NCTL ? tid - NSW * 64 : tid, nct = NCTL ? NCTL * 64 : NT;
+  uint16_t* planes = reinterpret_cast<uint16_t*>(xs);   // matrix-core tiles: [3][B][Ks]
+  const int pst = B * g.Ks;                             // values per plane
+  auto put_pair = [&](int i, int k, float a, float b) {
+    const uint16_t h0 = to_bf16(a), h1 = to_bf16(b);
+    a -= __uint_as_float((u32)h0 << 16);
+    b -= __uint_as_float((u32)h1 << 16);
+    const uint16_t m0_ = to_bf16(a), m1_ = to_bf16(b);
+    a -= __uint_as_float((u32)m0_ << 16);
+    b -= __uint_as_float((u32)m1_ << 16);
+    const uint16_t l0 = to_bf16(a), l1 = to_bf16(b);
+    u32* q = reinterpret_cast<u32*>(planes + i * g.Ks + k);
+    q[0] = (u32)h0 | ((u32)h1 << 16);
+    q[pst / 2] = (u32)m0_ | ((u32)m1_ << 16);
+    q[pst] = (u32)l0 | ((u32)l1 << 16);
+  };
+  float* mss = misc + 512;                              // matrix-core tiles: [NWAVE][B] sums of squares
+  auto stage_mf = [&](int s) -> bool {
+    const int k0 = s * g.Ks, kn = min(g.Ks, K - k0);
+    const int kfill = (kn + 31) & ~31;
+    // zeros: the padding columns of every lane, every column of absent batch lanes
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+      for (int k = (i >= p.b ? 0 : kn) + tid * 2; k < kfill; k += NT * 2) put_pair(i, k, 0.f, 0.f);
+    }
+    if (!ctl) return true;
+    const u32* gsl = gain ? reinterpret_cast<const u32*>(gain + k0) : nullptr;
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+      if (i >= p.b) continue;
+      float ss = 0.f;
+      auto use = [&](int k, float a, float b, u32 g2) {
+        ss += a * a + b * b;
+        if (gsl) { a *= bf16lo(g2); b *= bf16hi(g2); }
+        put_pair(i, k, a, b);
+      };
+      if (from_embed) {
+        const uint16_t* e = p.embed + (size_t)st.tok[i] * p.h + k0;
+        for (int k = ct * 2; k < kn; k += nct * 2) {
+          const u32 w2 = *reinterpret_cast<const u32*>(e + k);
+          use(k, bf16lo(w2), bf16hi(w2), gsl ? gsl[k >> 1] : 0u);
+        }
+      } else {
+        if (!wait_pairs<WBC>(p, st, ract, in_w + (u32)i * in_stride + (u32)k0, kn, gsl, use, ct, nct)) return false;
+      }
+      // Sum of squares so far: one partial per wave and lane in LDS (the stream keeps no
+      // registers for it).
+      const float wsum = wave_sum(ss);
+      if (lane == 0) mss[wave * B + i] = (s == 0 ? 0.f : mss[wave * B + i]) + wsum;
+    }
+    return true;
+  };
   auto stage = [&](int s, bool accumulate_ss, float* ssv) -> bool {
     const int k0 = s * g.Ks, kn = min(g.Ks, K - k0);
     const int kfill = (kn + 127) & ~127;
@@ -449,7 +537,9 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
   float ssv[B];
 #pragma unroll
   for (int i = 0; i < B; ++i) ssv[i] = 0.f;
-  if (g.nslab == 1) {
+  if constexpr (MF) {
+    ok = stage_mf(0);
+  } else if (g.nslab == 1) {
     ok = stage(0, gain != nullptr, ssv);
   } else if (gain) {
     // Whole-vector pass for the norm statistics, then stage slab 0.
@@ -492,7 +582,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
   }
   if (__syncthreads_or(!ok)) return false;
   if (tl && tid == 0) tl[1] = clock_now();
-  if (gain) {
+  if (!MF && gain) {
 #pragma unroll
     for (int i = 0; i < B; ++i) {
       float t = block_sum(ssv[i], misc, lane, wave);
@@ -501,23 +591,28 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
     scale_slab(0);
     __syncthreads();
   }
-  tap_slab(0);
+  if (!MF) tap_slab(0);
   if (tl && tid == 0) tl[2] = clock_now();
 
   // 3. Stream the weights: consume the ring in order, refilling each slot as it is used.
   for (int s = 0; s < g.nslab; ++s) {
     if (s > 0) {
       __syncthreads();
-      if (!stage(s, false, ssv)) ok = false;
-      if (__syncthreads_or(!ok)) return false;
-      scale_slab(s);
-      __syncthreads();
-      tap_slab(s);
+      if constexpr (MF) {
+        if (!stage_mf(s)) ok = false;
+        if (__syncthreads_or(!ok)) return false;
+      } else {
+        if (!stage(s, false, ssv)) ok = false;
+        if (__syncthreads_or(!ok)) return false;
+        scale_slab(s);
+        __syncthreads();
+        tap_slab(s);
+      }
       set_slab(s);
       cursor_at(ci, g, 0, wave);
 #pragma unroll
       for (int sl = 0; sl < U; ++sl) {
-        load_unit<NW>(ring[sl], g, ci, lane, op, ra, m0, m1, m2, nq, nk, zp);
+        load_unit<NW, MF>(ring[sl], g, ci, lane, op, ra, m0, m1, m2, nq, nk, zp);
         cursor_next(ci, g, wave);
       }
     }
@@ -527,17 +622,35 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
     float acc[B];
 #pragma unroll
     for (int i = 0; i < B; ++i) acc[i] = 0.f;
+    f32x4 acc4 = {0.f, 0.f, 0.f, 0.f};     // matrix-core tiles: C rows 4 (lane / 16) + r, column lane % 16
     for (int base = 0; base < units; base += U) {
 #pragma unroll
       for (int sl = 0; sl < U; ++sl) {
+        // Use the slot, then refill it: the refill then lands in the same registers (issued
+        // before the use, it would need other registers and a copy back that waits for it).
+        // The refill is unconditional (see load_unit).
+        const u32x4 w = ring[sl];
         if (base + sl < units) {
-          const u32x4 w = ring[sl];
-          load_unit<NW>(ring[sl], g, ci, lane, op, ra, m0, m1, m2, nq, nk, zp);
-          cursor_next(ci, g, wave);
           const int seg = cc.pt * g.SP + cc.sg;
           // Units past the slab's segments (the last K part may be short) were never loaded
           // and contribute nothing.
-          if (seg < g.nseg) {
+          if constexpr (MF) {
+            if (seg < g.nseg) {
+              const int j = lane & 15;
+              const int kk = seg * 32 + (lane >> 4) * 8;      // this lane's 8-column block
+              bf16x8 xh = {}, xm = {}, xl = {};
+              if (j < B) {
+                const uint16_t* pl = planes + j * g.Ks + kk;
+                xh = *reinterpret_cast<const bf16x8*>(pl);
+                xm = *reinterpret_cast<const bf16x8*>(pl + pst);
+                xl = *reinterpret_cast<const bf16x8*>(pl + 2 * pst);
+              }
+              const bf16x8 wa = __builtin_bit_cast(bf16x8, w);
+              acc4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, xl, acc4, 0, 0, 0);
+              acc4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, xm, acc4, 0, 0, 0);
+              acc4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, xh, acc4, 0, 0, 0);
+            }
+          } else if (seg < g.nseg) {
             const int kk = seg * 128 + (lane & 15) * 8;   // column within the slab
             const float w0 = bf16lo(w.x), w1 = bf16hi(w.x), w2 = bf16lo(w.y), w3 = bf16hi(w.y);
             const float w4 = bf16lo(w.z), w5 = bf16hi(w.z), w6 = bf16lo(w.w), w7 = bf16hi(w.w);
@@ -553,27 +666,69 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
             }
           }
           if (cc.sg == g.SP - 1) {
-            // Item finished: each 16-lane row sums its weight row; its first lane stores the
-            // part sum (added to earlier slabs' sums).
-            const int wr = cc.qd * 4 + (lane >> 4);
-            const bool writer = (lane & 15) == 0 && wr < g.nwr;
+            // Item finished: store the part sums (added to earlier slabs' sums).
+            if constexpr (MF) {
+              const int j = lane & 15;
 #pragma unroll
-            for (int i = 0; i < B; ++i) {
-              const float v = row16_sum(acc[i]);
-              acc[i] = 0.f;
-              if (writer) {
-                float* dst = rowacc + ((cc.pt * nr) * NW + wr) * B + i;
-                *dst = (s == 0) ? v : *dst + v;
+              for (int r = 0; r < 4; ++r) {
+                const int wr = cc.qd * 16 + 4 * (lane >> 4) + r;
+                if (j < B && wr < g.nwr) {
+                  float* dst = rowacc + ((cc.pt * nr) * NW + wr) * B + j;
+                  *dst = (s == 0) ? acc4[r] : *dst + acc4[r];
+                }
+              }
+              acc4 = f32x4{0.f, 0.f, 0.f, 0.f};
+            } else {
+              // Each 16-lane row sums its weight row; its first lane stores the part sum.
+              const int wr = cc.qd * 4 + (lane >> 4);
+              const bool writer = (lane & 15) == 0 && wr < g.nwr;
+#pragma unroll
+              for (int i = 0; i < B; ++i) {
+                const float v = row16_sum(acc[i]);
+                acc[i] = 0.f;
+                if (writer) {
+                  float* dst = rowacc + ((cc.pt * nr) * NW + wr) * B + i;
+                  *dst = (s == 0) ? v : *dst + v;
+                }
               }
             }
           }
           cursor_next(cc, g, wave);
         }
+        load_unit<NW, MF>(ring[sl], g, ci, lane, op, ra, m0, m1, m2, nq, nk, zp);
+        cursor_next(ci, g, wave);
       }
     }
   }
   __syncthreads();
   if (tl && tid == 0) tl[3] = clock_now();
+  if (MF && gain) {
+    // Matrix-core tiles: the norm's 1/rms, now that every slab has been seen, and the
+    // normalised input tap (re-read from the input words, still current this step).
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+      float t = 0.f;
+      for (int w = 0; w < NWAVE; ++w) t += mss[w * B + i];
+      rs[i] = 1.0f / sqrtf(t / (float)K + p.eps);
+    }
+    if (st.taps && ra == 0) {
+      const int off = (op == FM_OP_QKV) ? p.tap_a : (op == FM_OP_GU ? p.tap_a2 : 0);
+#pragma unroll
+      for (int i = 0; i < B; ++i) {
+        if (i >= p.b) continue;
+        float* t = (op == FM_OP_LM)
+                       ? st.taps + (size_t)p.L * p.b * p.tap_block + (size_t)i * p.h
+                       : st.taps + ((size_t)l * p.b + i) * p.tap_block + off;
+        for (int k = tid; k < K; k += NT) {
+          const float x = from_embed
+              ? __uint_as_float((u32)p.embed[(size_t)st.tok[i] * p.h + k] << 16)
+              : __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ract, (in_w + (u32)i * in_stride + (u32)k) * 8u,
+                                                                      0, CPOL_SC1));
+          t[k] = x * rs[i] * __uint_as_float((u32)gain[k] << 16);
+        }
+      }
+    }
+  }
 
   // 4. Epilogue, one output row per thread: K-part sums in order, residual adds, SiLU * up,
   //    tagged stores, taps, logits; the LM head also folds its rows into one packed argmax
@@ -590,6 +745,10 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
       for (int pt = 0; pt < KP0; ++pt) {
         y += rowacc[((pt * nr + rl) * NW) * B + i];
         if (NW == 2) up += rowacc[((pt * nr + rl) * NW + 1) * B + i];
+      }
+      if (MF && gain) {
+        y *= rs[i];
+        up *= rs[i];
       }
       switch (op) {
         case FM_OP_QKV:
@@ -643,23 +802,28 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
       if (lane == 0) wkeys[wave * B + i] = k;
     }
     __syncthreads();
-    if (tid == 0) {
-      u64 sink = 0;
-      for (int i = 0; i < p.b; ++i) {
-        u64 k = 0;
-        for (int w = 0; w < NWAVE; ++w) k = wkeys[w * B + i] > k ? wkeys[w * B + i] : k;
-        if (k) sink += __hip_atomic_fetch_max(p.amax + i, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
+    // One thread per batch lane folds the waves' keys into the step's maximum (all lanes'
+    // atomics in flight together), and waits until its atomic has been performed.
+    if (tid < p.b) {
+      u64 k = 0;
+      for (int w = 0; w < NWAVE; ++w) k = wkeys[w * B + tid] > k ? wkeys[w * B + tid] : k;
+      if (k) __hip_atomic_fetch_max(p.amax + tid, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       vm_wait0();
+    }
+    __syncthreads();
+    // The tile that arrives last (all maxima performed) writes the tokens and resets.
+    int* last = reinterpret_cast<int*>(misc + 8);
+    if (tid == 0) {
       const u32 old = __hip_atomic_fetch_add(p.lm_arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (old + (u32)(sink == 1234567ull) == (u32)p.n_lm_instr - 1u) {
-        for (int i = 0; i < p.b; ++i) {
-          const u64 k = __hip_atomic_load(p.amax + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          st.next_ids[i] = (int32_t)(0xFFFFFFFFu - (u32)(k & 0xFFFFFFFFull));
-          __hip_atomic_store(p.amax + i, (u64)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        __hip_atomic_store(p.lm_arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
+      const int is_last = old == (u32)p.n_lm_instr - 1u ? 1 : 0;
+      if (is_last) __hip_atomic_store(p.lm_arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      *last = is_last;
+    }
+    __syncthreads();
+    if (*last && tid < p.b) {
+      const u64 k = __hip_atomic_load(p.amax + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      st.next_ids[tid] = (int32_t)(0xFFFFFFFFu - (u32)(k & 0xFFFFFFFFull));
+      __hip_atomic_store(p.amax + tid, (u64)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
   __syncthreads();   // LDS is reused by the next instruction
@@ -851,11 +1015,10 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
     }
   }
 
-  // LDS: the slab region holds the merger's partials [G][nc][D + 2]; this item's working
-  // vectors live in the row-sum and residual regions behind it.
-  static_assert(GT * D + 2 * D + NWAVE * GT * (D + 2) <= ROWACC_FLOATS + RESID_FLOATS, "attention LDS");
-  float* cp = smem;
-  float* qs = smem + XSLAB_FLOATS;  // [G][D]
+  // LDS: the merger's partials at the start, this item's working vectors near the end.
+  static_assert(GT * D + 2 * D + NWAVE * GT * (D + 2) <= ATT_FLOATS, "attention LDS");
+  float* cp = smem;                 // [G][nc][D + 2], at most kMergeFloats
+  float* qs = smem + LDS_FLOATS - MISC_FLOATS - ATT_FLOATS;  // [G][D]
   float* ks = qs + GT * D;          // [D]
   float* vs = ks + D;               // [D]
   float* wst = vs + D;              // [NWAVE][GT][D + 2]

@@ -59,7 +59,7 @@ fm_status build_plan(const fm_model_cfg& c, int32_t nwg, Plan& p, std::string* w
     int32_t need = nkv * b;
     P = nwg;
     if (need > nwg / 2) P = nwg * ((need + nwg + nwg - 1) / nwg);
-    const int32_t cap = kSlabFloats / ((nh / nkv) * (d + 2));   // chunks per group
+    const int32_t cap = kMergeFloats / ((nh / nkv) * (d + 2));   // chunks per group
     if (cap >= 1 && P > need + (cap - 1) * nkv) P = need + (cap - 1) * nkv;
     if (P <= need) P = need + 1;
   }
