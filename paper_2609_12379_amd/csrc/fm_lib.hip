@@ -200,14 +200,9 @@ fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_k
     auto rows_max = [&](int64_t n) { return (n + nwg - 1) / nwg; };
     if (rows_max(hd) * Bt > RESID_FLOATS) { free_handle(h); return FM_ERR_CAPACITY; }
     const int64_t rowacc_cap = Bt >= 4 ? rowacc_floats<4>() : rowacc_floats<1>();
-    // rowacc holds [KP][rows][nw][B]; KP > 1 only when the tile has fewer than NWAVE row
-    // groups (4 weight rows per group, 16 on the matrix-core path of batched steps).
-    const int64_t grp = Bt >= 4 ? 16 : 4;
-    auto needs = [&](int64_t rows, int nw) {
-      const int64_t r = rows_max(rows), quads = (r * nw + grp - 1) / grp;
-      const int64_t kp = quads < NWAVE ? NWAVE / std::max<int64_t>(quads, 1) : 1;
-      return r * nw * Bt * kp;
-    };
+    // The row sums of a tile, [KP][rows][nw][B], must fit with one K part at least (the
+    // kernel uses more parts only while they fit).
+    auto needs = [&](int64_t rows, int nw) { return rows_max(rows) * nw * Bt; };
     if (needs(nqkv, 1) > rowacc_cap || needs(hd, 1) > rowacc_cap || needs(inter, 2) > rowacc_cap ||
         needs(V, 1) > rowacc_cap) {
       free_handle(h);

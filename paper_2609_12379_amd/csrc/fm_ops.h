@@ -362,13 +362,16 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
     g.kend = uni(g.k0 + kn);
     g.nseg = uni((kn + US::cols - 1) / US::cols);
     if (s == 0) {
-      // K parts are fixed for the whole tile (every slab splits its columns the same way,
-      // so each (row group, part) item stays with one wave and its row sums add up across
-      // slabs); a shorter last slab just leaves some parts empty.
+      // K parts: the fewest (1, 2, 4 or 8) that deal the (row group, part) items to the waves
+      // within 3% of even, as far as the row sums fit in LDS. They are fixed for the whole
+      // tile (every slab splits its columns the same way, so each item stays with one wave
+      // and its row sums add up across slabs); a shorter last slab leaves some parts empty.
       int kp = 1;
-      if (g.NQ < NSW) {
-        kp = NSW / g.NQ;
-        if (kp > g.nseg) kp = g.nseg;
+      for (int c = 1; c <= 8; c *= 2) {
+        if (c > g.nseg || c * nr * NW * B > rowacc_floats<B>()) break;
+        kp = c;
+        const int items = g.NQ * c, per = (items + NSW - 1) / NSW;
+        if (per * NSW * 100 <= items * 103) break;
       }
       g.KP = uni(kp);
       g.nitems = uni(g.NQ * g.KP);
