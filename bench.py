@@ -42,7 +42,7 @@ def kernel_source_hash() -> str:
 def profiled_traffic(config_name: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary of this workload, if
     it was taken on the current kernel sources (else None)."""
-    path = os.path.join(ROOT, "profiles", f"step_kernel_{config_name}_b1.md")
+    path = os.path.join(ROOT, "profiles", f"step_kernel_{config_name}.md")
     if not os.path.exists(path):
         return None
     fields = {}
