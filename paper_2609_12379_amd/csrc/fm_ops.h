@@ -399,19 +399,11 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
     cursor_next(ci, g, wave);
   }
 
-  constexpr int GP = 8;                  // gain pairs held in registers (K <= 8192)
-  u32 gpair[GP];
-  const bool gains_in_regs = !MF && gain && g.nslab == 1 && K <= GP * NT * 2;
-#pragma unroll
-  for (int jj = 0; jj < GP; ++jj) {
-    const int k = tid * 2 + jj * NT * 2;
-    gpair[jj] = (gains_in_regs && k < K) ? *reinterpret_cast<const u32*>(gain + k) : 0u;
-  }
-
-  // 2. Input: wait for the producers, then stage the values in LDS. VALU tiles hold the
-  //    normalised fp32 values. Matrix-core tiles hold x * g split into three bf16 planes
-  //    (hi + mid + lo = x * g to about 2^-24 relative); their 1/rms is applied to the
-  //    finished rows in the epilogue, since a slab sees only part of x.
+  // 2. Input: wait for the producers, then stage x * g (x times its RMSNorm gain, if any) in
+  //    LDS: fp32 for VALU tiles; three bf16 planes for matrix-core tiles (hi + mid + lo =
+  //    x * g to about 2^-24 relative). The norm's 1/rms is applied to the finished rows in the
+  //    epilogue: the sum of squares is gathered while staging, and no pass over the slab is
+  //    needed once it is known.
   bool ok = true;
   float rs[B];
 #pragma unroll
@@ -422,22 +414,27 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
   uint16_t* planes = reinterpret_cast<uint16_t*>(xs);   // matrix-core tiles: [3][B][Ks]
   const int pst = B * g.Ks;                             // values per plane
   auto put_pair = [&](int i, int k, float a, float b) {
-    const uint16_t h0 = to_bf16(a), h1 = to_bf16(b);
-    a -= __uint_as_float((u32)h0 << 16);
-    b -= __uint_as_float((u32)h1 << 16);
-    const uint16_t m0_ = to_bf16(a), m1_ = to_bf16(b);
-    a -= __uint_as_float((u32)m0_ << 16);
-    b -= __uint_as_float((u32)m1_ << 16);
-    const uint16_t l0 = to_bf16(a), l1 = to_bf16(b);
-    u32* q = reinterpret_cast<u32*>(planes + i * g.Ks + k);
-    q[0] = (u32)h0 | ((u32)h1 << 16);
-    q[pst / 2] = (u32)m0_ | ((u32)m1_ << 16);
-    q[pst] = (u32)l0 | ((u32)l1 << 16);
+    if constexpr (MF) {
+      const uint16_t h0 = to_bf16(a), h1 = to_bf16(b);
+      a -= __uint_as_float((u32)h0 << 16);
+      b -= __uint_as_float((u32)h1 << 16);
+      const uint16_t m0_ = to_bf16(a), m1_ = to_bf16(b);
+      a -= __uint_as_float((u32)m0_ << 16);
+      b -= __uint_as_float((u32)m1_ << 16);
+      const uint16_t l0 = to_bf16(a), l1 = to_bf16(b);
+      u32* q = reinterpret_cast<u32*>(planes + i * g.Ks + k);
+      q[0] = (u32)h0 | ((u32)h1 << 16);
+      q[pst / 2] = (u32)m0_ | ((u32)m1_ << 16);
+      q[pst] = (u32)l0 | ((u32)l1 << 16);
+    } else {
+      xs[i * g.Ks + k] = a;
+      xs[i * g.Ks + k + 1] = b;
+    }
   };
-  float* mss = misc + 512;                              // matrix-core tiles: [NWAVE][B] sums of squares
-  auto stage_mf = [&](int s) -> bool {
+  float* mss = misc + 512;                              // [NWAVE][B] partial sums of squares
+  auto stage = [&](int s) -> bool {
     const int k0 = s * g.Ks, kn = min(g.Ks, K - k0);
-    const int kfill = (kn + 31) & ~31;
+    const int kfill = (kn + US::cols - 1) & ~(US::cols - 1);
     // zeros: the padding columns of every lane, every column of absent batch lanes
 #pragma unroll
     for (int i = 0; i < B; ++i) {
@@ -463,108 +460,17 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
       } else {
         if (!wait_pairs<WBC>(p, st, ract, in_w + (u32)i * in_stride + (u32)k0, kn, gsl, use, ct, nct)) return false;
       }
-      // Sum of squares so far: one partial per wave and lane in LDS (the stream keeps no
-      // registers for it).
-      const float wsum = wave_sum(ss);
-      if (lane == 0) mss[wave * B + i] = (s == 0 ? 0.f : mss[wave * B + i]) + wsum;
-    }
-    return true;
-  };
-  auto stage = [&](int s, bool accumulate_ss, float* ssv) -> bool {
-    const int k0 = s * g.Ks, kn = min(g.Ks, K - k0);
-    const int kfill = (kn + 127) & ~127;
-#pragma unroll
-    for (int i = 0; i < B; ++i) {
-      float* dst = xs + i * g.Ks;
-      // zero padding (and absent batch lanes): any thread, disjoint from staged columns
-      if (i >= p.b) {
-        for (int k = tid; k < kn; k += NT) dst[k] = 0.f;
-      }
-      for (int k = kn + tid; k < kfill; k += NT) dst[k] = 0.f;
-      if (!ctl || i >= p.b) continue;
-      float ss = 0.f;
-      if (from_embed) {
-        const uint16_t* e = p.embed + (size_t)st.tok[i] * p.h + k0;
-        for (int k = ct * 2; k < kn; k += nct * 2) {
-          u32 w2 = *reinterpret_cast<const u32*>(e + k);
-          float a = bf16lo(w2), b = bf16hi(w2);
-          ss += a * a + b * b;
-          dst[k] = a; dst[k + 1] = b;
-        }
-      } else {
-        if (!wait_copy_t<WBC>(p, st, ract, in_w + (u32)i * in_stride + (u32)k0, kn, dst, ss, ct, nct)) return false;
-      }
-      if (accumulate_ss) {
-#pragma unroll
-        for (int ii = 0; ii < B; ++ii) if (ii == i) ssv[ii] += ss;   // static register index
+      if (gain) {
+        // Sum of squares so far: one partial per wave and lane in LDS (the stream keeps no
+        // registers for it).
+        const float wsum = wave_sum(ss);
+        if (lane == 0) mss[wave * B + i] = (s == 0 ? 0.f : mss[wave * B + i]) + wsum;
       }
     }
     return true;
-  };
-  auto scale_slab = [&](int s) {
-    if (!gain) return;
-    if (gains_in_regs) {
-#pragma unroll
-      for (int i = 0; i < B; ++i) {
-        float* dst = xs + i * g.Ks;
-#pragma unroll
-        for (int jj = 0; jj < GP; ++jj) {
-          const int k = tid * 2 + jj * NT * 2;
-          if (k < K) {
-            dst[k] = dst[k] * rs[i] * bf16lo(gpair[jj]);
-            dst[k + 1] = dst[k + 1] * rs[i] * bf16hi(gpair[jj]);
-          }
-        }
-      }
-      return;
-    }
-    const int k0 = s * g.Ks, kn = min(g.Ks, K - k0);
-#pragma unroll
-    for (int i = 0; i < B; ++i) {
-      float* dst = xs + i * g.Ks;
-      for (int k = tid; k < kn; k += NT) dst[k] = dst[k] * rs[i] * __uint_as_float((u32)gain[k0 + k] << 16);
-    }
-  };
-  auto tap_slab = [&](int s) {
-    if (!(st.taps && gain && ra == 0)) return;
-    const int k0 = s * g.Ks, kn = min(g.Ks, K - k0);
-    const int off = (op == FM_OP_QKV) ? p.tap_a : (op == FM_OP_GU ? p.tap_a2 : 0);
-    for (int i = 0; i < p.b; ++i) {
-      float* t = (op == FM_OP_LM)
-                     ? st.taps + (size_t)p.L * p.b * p.tap_block + (size_t)i * p.h
-                     : st.taps + ((size_t)l * p.b + i) * p.tap_block + off;
-      for (int k = tid; k < kn; k += NT) t[k0 + k] = xs[i * g.Ks + k];
-    }
   };
 
-  float ssv[B];
-#pragma unroll
-  for (int i = 0; i < B; ++i) ssv[i] = 0.f;
-  if constexpr (MF) {
-    ok = stage_mf(0);
-  } else if (g.nslab == 1) {
-    ok = stage(0, gain != nullptr, ssv);
-  } else if (gain) {
-    // Whole-vector pass for the norm statistics, then stage slab 0.
-    for (int i = 0; i < B && ok; ++i) {
-      if (i >= p.b || !ctl) continue;
-      float ss = 0.f;
-      if (from_embed) {
-        const uint16_t* e = p.embed + (size_t)st.tok[i] * p.h;
-        for (int k = ct * 2; k < K; k += nct * 2) {
-          u32 w2 = *reinterpret_cast<const u32*>(e + k);
-          float a = bf16lo(w2), b = bf16hi(w2);
-          ss += a * a + b * b;
-        }
-      } else {
-        ok = wait_copy_t<WBC>(p, st, ract, in_w + (u32)i * in_stride, K, nullptr, ss, ct, nct);
-      }
-      ssv[i] += ss;
-    }
-    if (ok) ok = stage(0, false, ssv);
-  } else {
-    ok = stage(0, false, ssv);
-  }
+  ok = stage(0);
   // Residual rows for the epilogue.
   if (ok && has_res && ctl) {
     for (int i = 0; i < B && ok; ++i) {
@@ -584,33 +490,14 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
     }
   }
   if (__syncthreads_or(!ok)) return false;
-  if (tl && tid == 0) tl[1] = clock_now();
-  if (!MF && gain) {
-#pragma unroll
-    for (int i = 0; i < B; ++i) {
-      float t = block_sum(ssv[i], misc, lane, wave);
-      rs[i] = 1.0f / sqrtf(t / (float)K + p.eps);
-    }
-    scale_slab(0);
-    __syncthreads();
-  }
-  if (!MF) tap_slab(0);
-  if (tl && tid == 0) tl[2] = clock_now();
+  if (tl && tid == 0) { tl[1] = clock_now(); tl[2] = tl[1]; }
 
   // 3. Stream the weights: consume the ring in order, refilling each slot as it is used.
   for (int s = 0; s < g.nslab; ++s) {
     if (s > 0) {
       __syncthreads();
-      if constexpr (MF) {
-        if (!stage_mf(s)) ok = false;
-        if (__syncthreads_or(!ok)) return false;
-      } else {
-        if (!stage(s, false, ssv)) ok = false;
-        if (__syncthreads_or(!ok)) return false;
-        scale_slab(s);
-        __syncthreads();
-        tap_slab(s);
-      }
+      if (!stage(s)) ok = false;
+      if (__syncthreads_or(!ok)) return false;
       set_slab(s);
       cursor_at(ci, g, 0, wave);
 #pragma unroll
@@ -705,9 +592,9 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
   }
   __syncthreads();
   if (tl && tid == 0) tl[3] = clock_now();
-  if (MF && gain) {
-    // Matrix-core tiles: the norm's 1/rms, now that every slab has been seen, and the
-    // normalised input tap (re-read from the input words, still current this step).
+  if (gain) {
+    // The norm's 1/rms, now that every slab has been seen, and the normalised input tap
+    // (re-read from the input words, still current this step).
 #pragma unroll
     for (int i = 0; i < B; ++i) {
       float t = 0.f;
@@ -749,7 +636,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
         y += rowacc[((pt * nr + rl) * NW) * B + i];
         if (NW == 2) up += rowacc[((pt * nr + rl) * NW + 1) * B + i];
       }
-      if (MF && gain) {
+      if (gain) {
         y *= rs[i];
         up *= rs[i];
       }
