@@ -173,9 +173,10 @@ size_t fm_tap_count(const fm_model_cfg *cfg);
 
 /* Instruction timeline: when buf (device uint64, 8 * fm_instruction_count(h) words) is
  * non-NULL, each step records per queued instruction q, at buf[8q..8q+7], the device
- * wall-clock ticks {start, inputs ready, prologue done, stream done, end, workgroup, 0, 0}.
+ * wall-clock ticks {start, inputs ready, prologue done, stream done, end, workgroup, a, b}.
  * For attention items the middle marks are: q/k/v ready, rotary and KV append done, partials
- * published; the span from there to the end is the group merge (last item of a group only).
+ * published; the span from there to the end is the group merge (last item of a group only);
+ * a = the item's slot passes done, b = its waves' partials gathered in LDS (0 for GEMV tiles).
  * Marks an instruction does not reach are 0. The ticks are from the 100 MHz constant clock,
  * read with s_memrealtime. These spans give the paper's busy fraction and tail spread
  * (Sec. 4.1, dependency gate). Pass NULL to turn the timeline off. */

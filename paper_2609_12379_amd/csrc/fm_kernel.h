@@ -50,7 +50,7 @@ __global__ __launch_bounds__(NT, 1) void step_kernel(const Params* __restrict__ 
     const int32_t* ins = P.instrs + 4 * (size_t)q;
     const int op = ins[0];
     u64* tl = st.timeline ? st.timeline + 8 * (size_t)q : nullptr;
-    if (tl && tid == 0) { tl[0] = clock_now(); tl[1] = 0; tl[2] = 0; tl[3] = 0; tl[5] = (u64)wg; }
+    if (tl && tid == 0) { tl[0] = clock_now(); tl[1] = 0; tl[2] = 0; tl[3] = 0; tl[5] = (u64)wg; tl[6] = 0; tl[7] = 0; }
     bool ok = true;
     if (op == FM_OP_ATTN) {
       ok = op_attn<D, GT>(P, st, ins, smem, tid, lane, wave, tl);

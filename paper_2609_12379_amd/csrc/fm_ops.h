@@ -387,7 +387,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
   float* resid = rowacc + rowacc_floats<B>();
   float* misc = smem + LDS_FLOATS - MISC_FLOATS;
 
-  // 1. Prefetch the first U units (and the RMSNorm gains), before waiting for the input.
+  // 1. Prefetch the first U units, before waiting for the input.
   const uint16_t* zp = zero_slot(p, wave, lane);
   constexpr int U = FM_RING;
   u32x4 ring[U];
@@ -729,8 +729,11 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
 // fit in P, so ragged lanes are balanced per step and no pass runs mostly empty.
 // An item reads its group's raw q (G heads), k and v and applies QK-norm and RoPE. The item
 // holding the group's last chunk also rounds the new k/v to bf16 and appends them at slot
-// kv_len. Each item runs an online softmax over its slots (Eq. 1; base-2 exponent with
-// log2(e)/sqrt(d) folded into q) and yields one partial (max, sum, weighted V) per head.
+// kv_len. Each item runs a softmax over its slots (Eq. 1; base-2 exponent with
+// log2(e)/sqrt(d) folded into q) a block of passes at a time: scores first, then a running
+// maximum shared by the wave, then exponentials and weighted V sums. It yields one partial
+// (max, sum, weighted V) per head. Lanes: LPS = d/8 lanes per slot, 8 dims (16 B of K and
+// of V) per lane, so a wave covers 64/LPS slots per pass and the K/V loads are contiguous.
 // The last chunk's item is the group's merger: the others publish their partials as tagged
 // words, and the merger combines them with its own in chunk order (log-sum-exp) and writes
 // the group's attention output.
@@ -763,16 +766,6 @@ __device__ __forceinline__ bool item_map(CParams& p, const Step& st, int j, int 
   return false;
 }
 
-__device__ __forceinline__ void sm_merge(float& m, float& l, float* acc, float mo, float lo, const float* acco) {
-  const float mn = fmaxf(m, mo);
-  const float a = (m == -INFINITY) ? 0.f : exp2f(m - mn);
-  const float b = (mo == -INFINITY) ? 0.f : exp2f(mo - mn);
-  l = l * a + lo * b;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) acc[e] = acc[e] * a + acco[e] * b;
-  m = mn;
-}
-
 // Sum within each 8-lane half-row; every lane of it gets the total (DPP).
 __device__ __forceinline__ float row8_sum(float s) {
   s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0xB1, 0xF, 0xF, false));   // quad [1,0,3,2]
@@ -802,20 +795,45 @@ __device__ __forceinline__ float lane_xor(float v, int lane) {
   return O == 8 ? lane_xor8(v) : (O == 16 ? lane_xor16(v, lane) : lane_xor32(v, lane));
 }
 
-// Merges the partials of the slot groups of a wave that share this lane's dims: lanes
-// (lane xor O) for O = LPS, 2 LPS, ..., 32.
+// Maximum over the slot groups of a wave (lanes lane xor O for O = LPS, 2 LPS, ..., 32): every
+// lane gets the wave's maximum.
+template <int O>
+__device__ __forceinline__ float max_slot_groups(float v, int lane) {
+  if constexpr (O <= 32) {
+    v = fmaxf(v, lane_xor<O>(v, lane));
+    return max_slot_groups<O * 2>(v, lane);
+  } else {
+    return v;
+  }
+}
+
+// Value of lane (lane + O) for the lanes whose bit O is clear, within each 2O-lane block
+// (other lanes get some other lane's value): one cross-lane move, no select.
+template <int O>
+__device__ __forceinline__ float lane_up(float v) {
+  static_assert(O == 8 || O == 16 || O == 32, "exchange distance");
+  if constexpr (O == 8) {
+    return lane_xor8(v);
+  } else if constexpr (O == 16) {
+    return __uint_as_float(__builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false)[1]);
+  } else {
+    return __uint_as_float(__builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false)[1]);
+  }
+}
+
+// Sums the softmax denominators and weighted V sums of a wave's slot groups (same lanes as
+// above) into the first group (lanes 0 .. LPS-1); other lanes end with partial sums. All
+// groups share one running maximum, so this is a plain sum.
 template <int O, int GT>
-__device__ __forceinline__ void merge_slot_groups(float (&m)[GT], float (&ls)[GT], float (&acc)[GT][8], int lane) {
+__device__ __forceinline__ void sum_slot_groups(float (&ls)[GT], float (&acc)[GT][8]) {
   if constexpr (O <= 32) {
 #pragma unroll
     for (int h = 0; h < GT; ++h) {
-      const float mo = lane_xor<O>(m[h], lane), lo = lane_xor<O>(ls[h], lane);
-      float ao[8];
+      ls[h] += lane_up<O>(ls[h]);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ao[e] = lane_xor<O>(acc[h][e], lane);
-      sm_merge(m[h], ls[h], acc[h], mo, lo, ao);
+      for (int e = 0; e < 8; ++e) acc[h][e] += lane_up<O>(acc[h][e]);
     }
-    merge_slot_groups<O * 2, GT>(m, ls, acc, lane);
+    sum_slot_groups<O * 2, GT>(ls, acc);
   }
 }
 
@@ -881,14 +899,14 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
   // Prefetch, before waiting for q: the first NPF passes of K/V, this lane's rotary row
   // and the QK-norm gains (none of them depend on this step's activations).
   u32x4 kr[NPF], vr[NPF];
-  auto issue = [&](int slot, int pass) {
+  auto kv_off = [&](int pass) {
     const int t = t0 + pass * SPP + wave * SPW + ssl;
-    const u32 off = (t < t_end) ? ((head_slot0 + (u32)t) * (u32)D + (u32)de) * 2u : 0xFFFFFFF0u;
-    kr[slot] = __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, CPOL_NT);
-    vr[slot] = __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, CPOL_NT);
+    return (t < t_end) ? ((head_slot0 + (u32)t) * (u32)D + (u32)de) * 2u : 0xFFFFFFF0u;
   };
+  auto issue_k = [&](int slot, int pass) { kr[slot] = __builtin_amdgcn_raw_buffer_load_b128(rk, kv_off(pass), 0, CPOL_NT); };
+  auto issue_v = [&](int slot, int pass) { vr[slot] = __builtin_amdgcn_raw_buffer_load_b128(rv, kv_off(pass), 0, CPOL_NT); };
 #pragma unroll
-  for (int s = 0; s < NPF; ++s) issue(s, s);
+  for (int s = 0; s < NPF; ++s) { issue_k(s, s); issue_v(s, s); }
   const int half = D / 2;
   const float* rt = p.rope + (size_t)st.pos[i] * half * 2;
   float2 rot = make_float2(1.f, 0.f);
@@ -973,21 +991,64 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
   }
-  auto update = [&](const float* kf, const float* vf, bool valid) {
+  // One block of NB slot passes (all wave-uniform): the scores of every slot in the block
+  // first, then one running maximum per head shared by the whole wave, then the exponentials
+  // and the weighted V sums. Because the maximum is the same in every lane, the wave's slot
+  // groups are combined at the end by plain sums, with no rescaling. ok[s] says the wave holds
+  // pass s; val[s] that this lane's slot in it is live. refill_k / refill_v(s) are called once
+  // pass s's K (V) registers are no longer needed.
+  auto block = [&](auto nbc, const u32x4* kw, const u32x4* vw, const bool* ok, const bool* val, auto refill_k,
+                   auto refill_v) {
+    constexpr int NB = decltype(nbc)::value;
+    float sc[NB][GT];
+#pragma unroll
+    for (int s = 0; s < NB; ++s) {
+#pragma unroll
+      for (int h = 0; h < GT; ++h) sc[s][h] = -INFINITY;
+      if (ok[s]) {
+        const u32x4 k = kw[s];
+        const float kf[8] = {bf16lo(k.x), bf16hi(k.x), bf16lo(k.y), bf16hi(k.y),
+                             bf16lo(k.z), bf16hi(k.z), bf16lo(k.w), bf16hi(k.w)};
+        refill_k(s);
+#pragma unroll
+        for (int h = 0; h < GT; ++h) {
+          if (h < G) {
+            float x = 0.f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x = fmaf(qr[h][e], kf[e], x);
+            x = (LPS == 16) ? row16_sum(x) : row8_sum(x);
+            sc[s][h] = val[s] ? x : -INFINITY;
+          }
+        }
+      }
+    }
 #pragma unroll
     for (int h = 0; h < GT; ++h) {
-      float sc = 0.f;
+      float bm = sc[0][h];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sc = fmaf(qr[h][e], kf[e], sc);
-      sc = (LPS == 16) ? row16_sum(sc) : row8_sum(sc);
-      if (valid && h < G) {
-        const float mn = fmaxf(m[h], sc);
-        const float a = (m[h] == -INFINITY) ? 0.f : exp2f(m[h] - mn);
-        const float pw = exp2f(sc - mn);
-        ls[h] = ls[h] * a + pw;
+      for (int s = 1; s < NB; ++s) bm = fmaxf(bm, sc[s][h]);
+      bm = max_slot_groups<LPS>(bm, lane);
+      const float mn = fmaxf(m[h], bm);
+      const float a = (m[h] == -INFINITY) ? 0.f : exp2f(m[h] - mn);
+      ls[h] *= a;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pw, vf[e], acc[h][e] * a);
-        m[h] = mn;
+      for (int e = 0; e < 8; ++e) acc[h][e] *= a;
+      m[h] = mn;
+    }
+#pragma unroll
+    for (int s = 0; s < NB; ++s) {
+      if (ok[s]) {
+        const u32x4 v = vw[s];
+        const float vf[8] = {bf16lo(v.x), bf16hi(v.x), bf16lo(v.y), bf16hi(v.y),
+                             bf16lo(v.z), bf16hi(v.z), bf16lo(v.w), bf16hi(v.w)};
+        refill_v(s);
+#pragma unroll
+        for (int h = 0; h < GT; ++h) {
+          const float pw = (sc[s][h] == -INFINITY) ? 0.f : exp2f(sc[s][h] - m[h]);
+          ls[h] += pw;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pw, vf[e], acc[h][e]);
+        }
       }
     }
   };
@@ -995,28 +1056,32 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
   const int n_arena = t_end - t0;
   const int npass = n_arena > 0 ? (n_arena + SPP - 1) / SPP : 0;
   for (int pb = 0; pb < npass; pb += NPF) {
+    bool ok[NPF], val[NPF];
 #pragma unroll
     for (int sl = 0; sl < NPF; ++sl) {
       const int pass = pb + sl;
-      if (pass < npass) {
-        const u32x4 kw = kr[sl], vw = vr[sl];
-        issue(sl, pass + NPF);
-        const int t = t0 + pass * SPP + wave * SPW + ssl;
-        const float kf[8] = {bf16lo(kw.x), bf16hi(kw.x), bf16lo(kw.y), bf16hi(kw.y),
-                             bf16lo(kw.z), bf16hi(kw.z), bf16lo(kw.w), bf16hi(kw.w)};
-        const float vf[8] = {bf16lo(vw.x), bf16hi(vw.x), bf16lo(vw.y), bf16hi(vw.y),
-                             bf16lo(vw.z), bf16hi(vw.z), bf16lo(vw.w), bf16hi(vw.w)};
-        update(kf, vf, t < t_end);
-      }
+      ok[sl] = pass < npass;
+      val[sl] = t0 + pass * SPP + wave * SPW + ssl < t_end;
     }
+    block(std::integral_constant<int, NPF>{}, kr, vr, ok, val,
+          [&](int sl) { issue_k(sl, pb + sl + NPF); }, [&](int sl) { issue_v(sl, pb + sl + NPF); });
   }
   if (is_last && wave == 0) {
-    float kf[8], vf[8];
+    // The new slot, as stored (bf16), in the first slot group of wave 0.
+    u32x4 kw1, vw1;
+    u32 kp[4], vp[4];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) { kf[e] = ks[de + e]; vf[e] = vs[de + e]; }
-    update(kf, vf, ssl == 0);
+    for (int j = 0; j < 4; ++j) {
+      kp[j] = (__float_as_uint(ks[de + 2 * j]) >> 16) | (__float_as_uint(ks[de + 2 * j + 1]) & 0xffff0000u);
+      vp[j] = (__float_as_uint(vs[de + 2 * j]) >> 16) | (__float_as_uint(vs[de + 2 * j + 1]) & 0xffff0000u);
+    }
+    kw1 = u32x4{kp[0], kp[1], kp[2], kp[3]};
+    vw1 = u32x4{vp[0], vp[1], vp[2], vp[3]};
+    const bool ok1[1] = {true}, val1[1] = {ssl == 0};
+    block(std::integral_constant<int, 1>{}, &kw1, &vw1, ok1, val1, [](int) {}, [](int) {});
   }
-  merge_slot_groups<LPS, GT>(m, ls, acc, lane);
+  if (tl && tid == 0) tl[6] = clock_now();
+  sum_slot_groups<LPS, GT>(ls, acc);
   if (ssl == 0) {
 #pragma unroll
     for (int h = 0; h < GT; ++h) {
@@ -1029,6 +1094,7 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
     }
   }
   __syncthreads();
+  if (tl && tid == 0) tl[7] = clock_now();
   // Merge the waves in order: the chunk's partial for each head. The merger keeps its own in
   // LDS (slot nc - 1 of cp); the other items publish theirs as tagged words.
   const int nh = p.nh;
