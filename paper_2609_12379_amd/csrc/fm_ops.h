@@ -206,13 +206,14 @@ __device__ __forceinline__ u32 ordered(float f) {
 // Lane layout: 16 lanes per weight row, 4 rows per wave load. A load ("unit") is 16 B per lane
 // = 128 columns of each of 4 rows ("quad"), so one reduction is a 4-step DPP sum inside each
 // 16-lane row and the activation chunk is an LDS broadcast. Quads are split along K into KP
-// parts when the tile has fewer quads than waves, so every wave keeps U = 16 loads in flight
-// whatever the tile's shape. Items (quad, part) are dealt to waves round-robin; a wave's units
+// parts when the tile has fewer quads than waves, so every wave keeps its U ring loads in
+// flight whatever the tile's shape. Items (quad, part) are dealt to waves round-robin; a wave's units
 // run item by item, SP segments per item. Part sums land in LDS and are added in part order
 // by the epilogue, so results do not depend on timing.
 //
-// Every ring slot issues exactly one global load (so the compiler counts loads in flight
-// exactly); lanes with nothing to load read a zeroed page instead.
+// Every ring slot issues exactly one global load per round (so the compiler counts loads in
+// flight exactly); lanes with nothing to load read a zeroed page instead. The last round
+// issues none.
 //
 // Batched tiles (B >= 4) run the products on the matrix cores instead (a skinny GEMM):
 // a unit is then 16 weight rows x 32 columns, loaded in the A-operand layout of
@@ -387,17 +388,21 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
   float* resid = rowacc + rowacc_floats<B>();
   float* misc = smem + LDS_FLOATS - MISC_FLOATS;
 
-  // 1. Prefetch the first U units, before waiting for the input.
+  // 1. Prefetch this wave's first U units, before waiting for the input.
   const uint16_t* zp = zero_slot(p, wave, lane);
   constexpr int U = FM_RING;
   u32x4 ring[U];
   GemvCursor ci;                          // issue cursor
-  cursor_at(ci, g, 0, wave);
-#pragma unroll
-  for (int sl = 0; sl < U; ++sl) {
+  auto refill = [&](int sl) {
     load_unit<NW, MF>(ring[sl], g, ci, lane, op, ra, m0, m1, m2, nq, nk, zp);
     cursor_next(ci, g, wave);
-  }
+  };
+  auto prefill = [&]() {
+    cursor_at(ci, g, 0, wave);
+#pragma unroll
+    for (int sl = 0; sl < U; ++sl) refill(sl);
+  };
+  prefill();
 
   // 2. Input: wait for the producers, then stage x * g (x times its RMSNorm gain, if any) in
   //    LDS: fp32 for VALU tiles; three bf16 planes for matrix-core tiles (hi + mid + lo =
@@ -499,12 +504,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
       if (!stage(s)) ok = false;
       if (__syncthreads_or(!ok)) return false;
       set_slab(s);
-      cursor_at(ci, g, 0, wave);
-#pragma unroll
-      for (int sl = 0; sl < U; ++sl) {
-        load_unit<NW, MF>(ring[sl], g, ci, lane, op, ra, m0, m1, m2, nq, nk, zp);
-        cursor_next(ci, g, wave);
-      }
+      prefill();
     }
     const int units = uni(g.items_w * g.SP);
     GemvCursor cc;                        // consume cursor
@@ -513,82 +513,89 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
 #pragma unroll
     for (int i = 0; i < B; ++i) acc[i] = 0.f;
     f32x4 acc4 = {0.f, 0.f, 0.f, 0.f};     // matrix-core tiles: C rows 4 (lane / 16) + r, column lane % 16
-    for (int base = 0; base < units; base += U) {
+    // Each round consumes the U slots in order and refills each one after its use (the refill
+    // then lands in the same registers; issued before the use, it would need other registers
+    // and a copy back that waits for it). Refills are unconditional (see load_unit), except
+    // that the last round only drains the ring: a refill there would load nothing the tile
+    // needs, and the epilogue, which reuses the ring's registers, would wait for it to land.
+    // (Refilling only the units that exist in the round before costs more: the compiler then
+    // drains the ring at every wait.)
+    auto consume = [&](const u32x4 w) {
+      const int seg = cc.pt * g.SP + cc.sg;
+      // Units past the slab's segments (the last K part may be short) were never loaded
+      // and contribute nothing.
+      if constexpr (MF) {
+        if (seg < g.nseg) {
+          const int j = lane & 15;
+          const int kk = seg * 32 + (lane >> 4) * 8;      // this lane's 8-column block
+          bf16x8 xh = {}, xm = {}, xl = {};
+          if (j < B) {
+            const uint16_t* pl = planes + j * g.Ks + kk;
+            xh = *reinterpret_cast<const bf16x8*>(pl);
+            xm = *reinterpret_cast<const bf16x8*>(pl + pst);
+            xl = *reinterpret_cast<const bf16x8*>(pl + 2 * pst);
+          }
+          const bf16x8 wa = __builtin_bit_cast(bf16x8, w);
+          acc4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, xl, acc4, 0, 0, 0);
+          acc4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, xm, acc4, 0, 0, 0);
+          acc4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, xh, acc4, 0, 0, 0);
+        }
+      } else if (seg < g.nseg) {
+        const int kk = seg * 128 + (lane & 15) * 8;   // column within the slab
+        const float w0 = bf16lo(w.x), w1 = bf16hi(w.x), w2 = bf16lo(w.y), w3 = bf16hi(w.y);
+        const float w4 = bf16lo(w.z), w5 = bf16hi(w.z), w6 = bf16lo(w.w), w7 = bf16hi(w.w);
+#pragma unroll
+        for (int i = 0; i < B; ++i) {
+          const float4 xa = *reinterpret_cast<const float4*>(xs + i * g.Ks + kk);
+          const float4 xb = *reinterpret_cast<const float4*>(xs + i * g.Ks + kk + 4);
+          float t0 = w0 * xa.x, t1 = w1 * xa.y;
+          t0 = fmaf(w2, xa.z, t0); t1 = fmaf(w3, xa.w, t1);
+          t0 = fmaf(w4, xb.x, t0); t1 = fmaf(w5, xb.y, t1);
+          t0 = fmaf(w6, xb.z, t0); t1 = fmaf(w7, xb.w, t1);
+          acc[i] += t0 + t1;
+        }
+      }
+      if (cc.sg == g.SP - 1) {
+        // Item finished: store the part sums (added to earlier slabs' sums).
+        if constexpr (MF) {
+          const int j = lane & 15;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int wr = cc.qd * 16 + 4 * (lane >> 4) + r;
+            if (j < B && wr < g.nwr) {
+              float* dst = rowacc + ((cc.pt * nr) * NW + wr) * B + j;
+              *dst = (s == 0) ? acc4[r] : *dst + acc4[r];
+            }
+          }
+          acc4 = f32x4{0.f, 0.f, 0.f, 0.f};
+        } else {
+          // Each 16-lane row sums its weight row; its first lane stores the part sum.
+          const int wr = cc.qd * 4 + (lane >> 4);
+          const bool writer = (lane & 15) == 0 && wr < g.nwr;
+#pragma unroll
+          for (int i = 0; i < B; ++i) {
+            const float v = row16_sum(acc[i]);
+            acc[i] = 0.f;
+            if (writer) {
+              float* dst = rowacc + ((cc.pt * nr) * NW + wr) * B + i;
+              *dst = (s == 0) ? v : *dst + v;
+            }
+          }
+        }
+      }
+      cursor_next(cc, g, wave);
+    };
+    int base = 0;
+    for (; base + U < units; base += U) {
 #pragma unroll
       for (int sl = 0; sl < U; ++sl) {
-        // Use the slot, then refill it: the refill then lands in the same registers (issued
-        // before the use, it would need other registers and a copy back that waits for it).
-        // The refill is unconditional (see load_unit).
-        const u32x4 w = ring[sl];
-        if (base + sl < units) {
-          const int seg = cc.pt * g.SP + cc.sg;
-          // Units past the slab's segments (the last K part may be short) were never loaded
-          // and contribute nothing.
-          if constexpr (MF) {
-            if (seg < g.nseg) {
-              const int j = lane & 15;
-              const int kk = seg * 32 + (lane >> 4) * 8;      // this lane's 8-column block
-              bf16x8 xh = {}, xm = {}, xl = {};
-              if (j < B) {
-                const uint16_t* pl = planes + j * g.Ks + kk;
-                xh = *reinterpret_cast<const bf16x8*>(pl);
-                xm = *reinterpret_cast<const bf16x8*>(pl + pst);
-                xl = *reinterpret_cast<const bf16x8*>(pl + 2 * pst);
-              }
-              const bf16x8 wa = __builtin_bit_cast(bf16x8, w);
-              acc4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, xl, acc4, 0, 0, 0);
-              acc4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, xm, acc4, 0, 0, 0);
-              acc4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, xh, acc4, 0, 0, 0);
-            }
-          } else if (seg < g.nseg) {
-            const int kk = seg * 128 + (lane & 15) * 8;   // column within the slab
-            const float w0 = bf16lo(w.x), w1 = bf16hi(w.x), w2 = bf16lo(w.y), w3 = bf16hi(w.y);
-            const float w4 = bf16lo(w.z), w5 = bf16hi(w.z), w6 = bf16lo(w.w), w7 = bf16hi(w.w);
-#pragma unroll
-            for (int i = 0; i < B; ++i) {
-              const float4 xa = *reinterpret_cast<const float4*>(xs + i * g.Ks + kk);
-              const float4 xb = *reinterpret_cast<const float4*>(xs + i * g.Ks + kk + 4);
-              float t0 = w0 * xa.x, t1 = w1 * xa.y;
-              t0 = fmaf(w2, xa.z, t0); t1 = fmaf(w3, xa.w, t1);
-              t0 = fmaf(w4, xb.x, t0); t1 = fmaf(w5, xb.y, t1);
-              t0 = fmaf(w6, xb.z, t0); t1 = fmaf(w7, xb.w, t1);
-              acc[i] += t0 + t1;
-            }
-          }
-          if (cc.sg == g.SP - 1) {
-            // Item finished: store the part sums (added to earlier slabs' sums).
-            if constexpr (MF) {
-              const int j = lane & 15;
-#pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                const int wr = cc.qd * 16 + 4 * (lane >> 4) + r;
-                if (j < B && wr < g.nwr) {
-                  float* dst = rowacc + ((cc.pt * nr) * NW + wr) * B + j;
-                  *dst = (s == 0) ? acc4[r] : *dst + acc4[r];
-                }
-              }
-              acc4 = f32x4{0.f, 0.f, 0.f, 0.f};
-            } else {
-              // Each 16-lane row sums its weight row; its first lane stores the part sum.
-              const int wr = cc.qd * 4 + (lane >> 4);
-              const bool writer = (lane & 15) == 0 && wr < g.nwr;
-#pragma unroll
-              for (int i = 0; i < B; ++i) {
-                const float v = row16_sum(acc[i]);
-                acc[i] = 0.f;
-                if (writer) {
-                  float* dst = rowacc + ((cc.pt * nr) * NW + wr) * B + i;
-                  *dst = (s == 0) ? v : *dst + v;
-                }
-              }
-            }
-          }
-          cursor_next(cc, g, wave);
-        }
-        load_unit<NW, MF>(ring[sl], g, ci, lane, op, ra, m0, m1, m2, nq, nk, zp);
-        cursor_next(ci, g, wave);
+        consume(ring[sl]);
+        refill(sl);
       }
     }
+#pragma unroll
+    for (int sl = 0; sl < U; ++sl)
+      if (base + sl < units) consume(ring[sl]);
   }
   __syncthreads();
   if (tl && tid == 0) tl[3] = clock_now();
