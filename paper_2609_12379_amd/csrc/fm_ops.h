@@ -847,7 +847,7 @@ __device__ __forceinline__ void sum_slot_groups(float (&ls)[GT], float (&acc)[GT
 // The merger of (lane i, KV head g): waits for the tagged partials of chunks 0..nc-2 of each
 // of the group's heads (staged into cp next to its own chunk nc-1, already in LDS), combines
 // them in chunk order (log-sum-exp) and writes the attention output of the G query heads.
-template <int D>
+template <int D, int GT>
 __device__ __forceinline__ bool merge_group(CParams& p, const Step& st, int l, int i, int g, int nc, float* cp,
                                             int tid) {
   const int G = p.G, nh = p.nh, row = D + 2;
@@ -868,14 +868,24 @@ __device__ __forceinline__ bool merge_group(CParams& p, const Step& st, int l, i
   for (int u = tid; u < G * D; u += NT) {
     const int h = u / D, e = u % D;
     const float* src = cp + h * per_head;
-    float M = -INFINITY;
-    for (int cc = 0; cc < nc; ++cc) M = fmaxf(M, src[cc * row + D]);
-    float den = 0.f, num = 0.f;
-    for (int cc = 0; cc < nc; ++cc) {
+    // Grouped-query kernels unroll the chunk loops so that the LDS reads of several chunks
+    // are in flight together (measured faster there, not with one head per group); the sums
+    // run in chunk order either way.
+    float M = -INFINITY, den = 0.f, num = 0.f;
+    auto add_chunk = [&](int cc) {
       const float* pc = src + cc * row;
       const float f = exp2f(pc[D] - M);
       den += f * pc[D + 1];
       num += f * pc[e];
+    };
+    if constexpr (GT >= 2) {
+#pragma unroll 8
+      for (int cc = 0; cc < nc; ++cc) M = fmaxf(M, src[cc * row + D]);
+#pragma unroll 8
+      for (int cc = 0; cc < nc; ++cc) add_chunk(cc);
+    } else {
+      for (int cc = 0; cc < nc; ++cc) M = fmaxf(M, src[cc * row + D]);
+      for (int cc = 0; cc < nc; ++cc) add_chunk(cc);
     }
     const float o = num / den;
     st_tag(p.act + obase + (u32)((g * G + h) * D + e), o, st.epoch);
@@ -1130,7 +1140,7 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
     }
   }
   if (tl && tid == 0) tl[3] = clock_now();
-  if (is_last && !merge_group<D>(p, st, l, i, g, nc, cp, tid)) return false;
+  if (is_last && !merge_group<D, GT>(p, st, l, i, g, nc, cp, tid)) return false;
   __syncthreads();   // LDS is reused by the next instruction
   return true;
 }
