@@ -746,18 +746,21 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
 // the group's attention output.
 
 // Chunk length of this step (see above); spp is the pass width.
-__device__ __forceinline__ int chunk_len(CParams& p, const Step& st, int spp) {
+// gran (<= spp) is the work granularity of one wave: chunks shorter than half a pass are
+// rounded to it instead (short contexts then keep many items, each on a few waves).
+__device__ __forceinline__ int chunk_len(CParams& p, const Step& st, int spp, int gran) {
   long long total = 0;
   for (int ii = 0; ii < p.b; ++ii) total += st.kvl[ii] + 1;
   total *= p.nkv;
   const long long denom = p.P - p.nkv * p.b;
   const int T0 = (int)((total + denom - 1) / denom);
-  return ((T0 + spp - 1) / spp) * spp;
+  const int q = (2 * T0 <= spp) ? gran : spp;
+  return ((T0 + q - 1) / q) * q;
 }
 
-__device__ __forceinline__ bool item_map(CParams& p, const Step& st, int j, int spp, int& i, int& g, int& c,
-                                         int& nc, int& t0, int& t1) {
-  const int T = chunk_len(p, st, spp);
+__device__ __forceinline__ bool item_map(CParams& p, const Step& st, int j, int spp, int gran, int& i, int& g,
+                                         int& c, int& nc, int& t0, int& t1) {
+  const int T = chunk_len(p, st, spp, gran);
   int idx = j;
   for (int ii = 0; ii < p.b; ++ii) {
     const int W = st.kvl[ii] + 1;
@@ -897,10 +900,16 @@ __device__ __forceinline__ bool merge_group(CParams& p, const Step& st, int l, i
 template <int D, int GT>
 __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_t* ins, float* smem, int tid,
                                         int lane, int wave, u64* tl) {
-  constexpr int LPS = D / 8, SPW = 64 / LPS, SPP = SPW * NWAVE, NPF = 4;
+  // Grouped-query kernels with d = 64 (GT >= 2) run the scores and the weighted V sums on the
+  // matrix cores in tiles of 16 slots per wave (pass width 128). The transposed V operand costs
+  // four 2-byte loads per 16 dims; at d = 128 that outweighed the gain (measured), so those
+  // kernels, and one-head-per-group kernels, use the VALU.
+  constexpr bool MFA = GT >= 2 && D == 64;
+  constexpr int LPS = D / 8, SPW = 64 / LPS, SPP = MFA ? 16 * NWAVE : SPW * NWAVE, NPF = 4;
+  constexpr int KB = D / 32, DB = D / 16;   // 32-dim blocks (scores), 16-dim blocks (V sums)
   const int l = uni(ins[1]), j = uni(ins[2]);
   int i, g, c, nc, t0, t1;
-  if (!item_map(p, st, j, SPP, i, g, c, nc, t0, t1)) return true;
+  if (!item_map(p, st, j, SPP, MFA ? 16 : SPP, i, g, c, nc, t0, t1)) return true;
   i = uni(i); g = uni(g); c = uni(c); nc = uni(nc); t0 = uni(t0); t1 = uni(t1);
   const int G = p.G;
   const int kvl = uni(st.kvl[i]);
@@ -913,17 +922,51 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
   const __amdgpu_buffer_rsrc_t rv = rsrc(Lw.vc, arena_bytes);
   const u32 head_slot0 = ((u32)i * p.nkv + (u32)g) * (u32)p.max_ctx;
 
-  // Prefetch, before waiting for q: the first NPF passes of K/V, this lane's rotary row
-  // and the QK-norm gains (none of them depend on this step's activations).
-  u32x4 kr[NPF], vr[NPF];
+  // Prefetch, before waiting for q: the first K/V of this wave (NPF passes, or two tiles),
+  // this lane's rotary row and the QK-norm gains (none of them depend on this step's
+  // activations).
+  u32x4 kr[MFA ? 1 : NPF], vr[MFA ? 1 : NPF];
   auto kv_off = [&](int pass) {
     const int t = t0 + pass * SPP + wave * SPW + ssl;
     return (t < t_end) ? ((head_slot0 + (u32)t) * (u32)D + (u32)de) * 2u : 0xFFFFFFF0u;
   };
   auto issue_k = [&](int slot, int pass) { kr[slot] = __builtin_amdgcn_raw_buffer_load_b128(rk, kv_off(pass), 0, CPOL_NT); };
   auto issue_v = [&](int slot, int pass) { vr[slot] = __builtin_amdgcn_raw_buffer_load_b128(rv, kv_off(pass), 0, CPOL_NT); };
+  // Matrix-core tiles: 16 slots s0 .. s0 + 15. K in the A-operand layout of the score product
+  // (lane l: slot s0 + l % 16, dims 32 kb + 8 (l / 16) .. + 8: one 16-byte load per block);
+  // V transposed, in the A-operand layout of the V sums (lane l: dim 16 db + l % 16 of slots
+  // s0 + 4 (l / 16) .. + 4: four 2-byte loads per block, packed two to a register). Slots past
+  // the chunk load zeros (out-of-range offsets).
+  u32x4 kA[MFA ? KB : 1], kB2[MFA ? KB : 1];
+  u32 vA[MFA ? DB : 1][2], vB2[MFA ? DB : 1][2];
+  auto tile_load = [&](u32x4* kt, u32 (*vt)[2], int s0) {
+    const int tk = s0 + (lane & 15);
 #pragma unroll
-  for (int s = 0; s < NPF; ++s) { issue_k(s, s); issue_v(s, s); }
+    for (int kb = 0; kb < KB; ++kb)
+      kt[kb] = __builtin_amdgcn_raw_buffer_load_b128(
+          rk, tk < t_end ? ((head_slot0 + (u32)tk) * (u32)D + (u32)(32 * kb + 8 * (lane >> 4))) * 2u : 0xFFFFFFF0u, 0,
+          CPOL_NT);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      u32 h[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int tv = s0 + 4 * (lane >> 4) + r;
+        h[r] = __builtin_amdgcn_raw_buffer_load_b16(
+            rv, tv < t_end ? ((head_slot0 + (u32)tv) * (u32)D + (u32)(16 * db + (lane & 15))) * 2u : 0xFFFFFFF0u, 0,
+            CPOL_NT);
+      }
+      vt[db][0] = h[0] | (h[1] << 16);
+      vt[db][1] = h[2] | (h[3] << 16);
+    }
+  };
+  if constexpr (MFA) {
+    tile_load(kA, vA, t0 + 16 * wave);
+    tile_load(kB2, vB2, t0 + 16 * (wave + NWAVE));
+  } else {
+#pragma unroll
+    for (int s = 0; s < NPF; ++s) { issue_k(s, s); issue_v(s, s); }
+  }
   const int half = D / 2;
   const float* rt = p.rope + (size_t)st.pos[i] * half * 2;
   float2 rot = make_float2(1.f, 0.f);
@@ -942,6 +985,7 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
 
   // LDS: the merger's partials at the start, this item's working vectors near the end.
   static_assert(GT * D + 2 * D + NWAVE * GT * (D + 2) <= ATT_FLOATS, "attention LDS");
+  static_assert(kMergeFloats + 3 * KB * 64 * 4 <= LDS_FLOATS - MISC_FLOATS - ATT_FLOATS, "q planes in LDS");
   float* cp = smem;                 // [G][nc][D + 2], at most kMergeFloats
   float* qs = smem + LDS_FLOATS - MISC_FLOATS - ATT_FLOATS;  // [G][D]
   float* ks = qs + GT * D;          // [D]
@@ -996,117 +1040,253 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
     __syncthreads();
   }
 
-  float qr[GT][8];
+  if constexpr (MFA) {
+    // q as the B operand of the score product S^T = K Q^T (v_mfma_f32_16x16x32_bf16): lane l
+    // holds head l % 16 (zero past G) at dims 32 kb + 8 (l / 16) .. + 8, split into three bf16
+    // planes (hi + mid + lo = q to about 2^-24 relative), so the scores keep fp32 precision.
+    // The same for every wave: built once in LDS, [plane][kb][lane] 16 bytes each.
+    u32x4* qpl = reinterpret_cast<u32x4*>(smem + kMergeFloats);
+    for (int u = tid; u < KB * 64; u += NT) {
+      const int kb = u / 64, ln = u % 64, h = ln & 15, d0 = 32 * kb + 8 * (ln >> 4);
+      u32 w[3][4];
 #pragma unroll
-  for (int h = 0; h < GT; ++h)
+      for (int e2 = 0; e2 < 4; ++e2) {
+        u32 hv[2], mv[2], lv[2];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) qr[h][e] = (h < G) ? qs[h * D + de + e] * p.q_scale : 0.f;
-  float m[GT], ls[GT], acc[GT][8];
+        for (int q2 = 0; q2 < 2; ++q2) {
+          float x = (h < G) ? qs[h * D + d0 + 2 * e2 + q2] * p.q_scale : 0.f;
+          const uint16_t hi = to_bf16(x);
+          x -= __uint_as_float((u32)hi << 16);
+          const uint16_t mi = to_bf16(x);
+          x -= __uint_as_float((u32)mi << 16);
+          hv[q2] = hi; mv[q2] = mi; lv[q2] = to_bf16(x);
+        }
+        w[0][e2] = hv[0] | (hv[1] << 16);
+        w[1][e2] = mv[0] | (mv[1] << 16);
+        w[2][e2] = lv[0] | (lv[1] << 16);
+      }
 #pragma unroll
-  for (int h = 0; h < GT; ++h) {
-    m[h] = -INFINITY; ls[h] = 0.f;
+      for (int pl = 0; pl < 3; ++pl) qpl[(pl * KB + kb) * 64 + ln] = u32x4{w[pl][0], w[pl][1], w[pl][2], w[pl][3]};
+    }
+    __syncthreads();
+    // Per lane: head l % 16; running maximum m (the same in the lane's four groups), partial
+    // denominator ls over its slots, and O^T blocks (dims 16 db + 4 (l / 16) + r).
+    float m = -INFINITY, ls = 0.f;
+    f32x4 o[DB];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
-  }
-  // One block of NB slot passes (all wave-uniform): the scores of every slot in the block
-  // first, then one running maximum per head shared by the whole wave, then the exponentials
-  // and the weighted V sums. Because the maximum is the same in every lane, the wave's slot
-  // groups are combined at the end by plain sums, with no rescaling. ok[s] says the wave holds
-  // pass s; val[s] that this lane's slot in it is live. refill_k / refill_v(s) are called once
-  // pass s's K (V) registers are no longer needed.
-  auto block = [&](auto nbc, const u32x4* kw, const u32x4* vw, const bool* ok, const bool* val, auto refill_k,
-                   auto refill_v) {
-    constexpr int NB = decltype(nbc)::value;
-    float sc[NB][GT];
+    for (int db = 0; db < DB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // One tile: scores S^T (rows = slots 4 (l / 16) + r, columns = heads), a running maximum
+    // per head across the wave, then O^T += V^T P^T on v_mfma_f32_16x16x16_bf16, whose B
+    // operand (slots 4 (l / 16) .. + 4 of head l % 16) is the score tile's own C layout. P is
+    // split into three bf16 planes like q.
+    typedef short s16x4 __attribute__((ext_vector_type(4)));
+    auto tile = [&](const u32x4* kt, const u32 (*vt)[2], auto live_row) {
+      f32x4 sc4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int s = 0; s < NB; ++s) {
+      for (int kb = 0; kb < KB; ++kb) {
+        const bf16x8 a = __builtin_bit_cast(bf16x8, kt[kb]);
 #pragma unroll
-      for (int h = 0; h < GT; ++h) sc[s][h] = -INFINITY;
-      if (ok[s]) {
-        const u32x4 k = kw[s];
-        const float kf[8] = {bf16lo(k.x), bf16hi(k.x), bf16lo(k.y), bf16hi(k.y),
-                             bf16lo(k.z), bf16hi(k.z), bf16lo(k.w), bf16hi(k.w)};
-        refill_k(s);
+        for (int pl = 2; pl >= 0; --pl)
+          sc4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, qpl[(pl * KB + kb) * 64 + lane]),
+                                                        sc4, 0, 0, 0);
+      }
+      const bool head_live = (lane & 15) < G;
+      float sc[4];
 #pragma unroll
-        for (int h = 0; h < GT; ++h) {
-          if (h < G) {
-            float x = 0.f;
+      for (int r = 0; r < 4; ++r) sc[r] = (head_live && live_row(r)) ? sc4[r] : -INFINITY;
+      float mt = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+      mt = fmaxf(mt, lane_xor<16>(mt, lane));
+      mt = fmaxf(mt, lane_xor<32>(mt, lane));
+      const float mn = fmaxf(m, mt);
+      const float a = (m == -INFINITY) ? 0.f : exp2f(m - mn);
+      ls *= a;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) x = fmaf(qr[h][e], kf[e], x);
-            x = (LPS == 16) ? row16_sum(x) : row8_sum(x);
-            sc[s][h] = val[s] ? x : -INFINITY;
+      for (int db = 0; db < DB; ++db) o[db] *= a;
+      m = mn;
+      s16x4 ph, pm, pl;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float x = (sc[r] == -INFINITY) ? 0.f : exp2f(sc[r] - mn);
+        ls += x;
+        const uint16_t hi = to_bf16(x);
+        x -= __uint_as_float((u32)hi << 16);
+        const uint16_t mi = to_bf16(x);
+        x -= __uint_as_float((u32)mi << 16);
+        const uint16_t lo = to_bf16(x);
+        ph[r] = (short)hi; pm[r] = (short)mi; pl[r] = (short)lo;
+      }
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const s16x4 va = {(short)(vt[db][0] & 0xffffu), (short)(vt[db][0] >> 16), (short)(vt[db][1] & 0xffffu),
+                          (short)(vt[db][1] >> 16)};
+        o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pl, o[db], 0, 0, 0);
+        o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pm, o[db], 0, 0, 0);
+        o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, ph, o[db], 0, 0, 0);
+      }
+    };
+    if (tl && tid == 0) tl[2] = clock_now();
+    // This wave's tiles: 16-slot tiles wave, wave + 8, ... of the chunk, two in flight.
+    const int n_arena = t_end - t0;
+    const int ntile = n_arena > 16 * wave ? (n_arena - 16 * wave + SPP - 1) / SPP : 0;
+    for (int k = 0; k < ntile; k += 2) {
+      {
+        const int s0 = t0 + 16 * (wave + NWAVE * k);
+        tile(kA, vA, [&](int r) { return s0 + 4 * (lane >> 4) + r < t_end; });
+        if (k + 2 < ntile) tile_load(kA, vA, t0 + 16 * (wave + NWAVE * (k + 2)));
+      }
+      if (k + 1 < ntile) {
+        const int s0 = t0 + 16 * (wave + NWAVE * (k + 1));
+        tile(kB2, vB2, [&](int r) { return s0 + 4 * (lane >> 4) + r < t_end; });
+        if (k + 3 < ntile) tile_load(kB2, vB2, t0 + 16 * (wave + NWAVE * (k + 3)));
+      }
+    }
+    if (is_last && wave == 0) {
+      // The new slot, as stored (bf16), folded into wave 0's running state on the VALU: its
+      // score for each head (a wave sum over the dims), then the usual update of this lane's
+      // head. The denominator counts it once, in the first lane group.
+      float s_new = -INFINITY;
+      for (int hh = 0; hh < G; ++hh) {
+        float x = qs[hh * D + lane] * p.q_scale * ks[lane];
+        if (D > 64) x = fmaf(qs[hh * D + lane + 64] * p.q_scale, ks[lane + 64], x);
+        x = wave_sum(x);
+        if ((lane & 15) == hh) s_new = x;
+      }
+      const float mn = fmaxf(m, s_new);
+      const float a = (m == -INFINITY) ? 0.f : exp2f(m - mn);
+      const float pw = (s_new == -INFINITY) ? 0.f : exp2f(s_new - mn);
+      ls = ls * a + (((lane >> 4) == 0) ? pw : 0.f);
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[db][r] = fmaf(pw, vs[16 * db + 4 * (lane >> 4) + r], o[db][r] * a);
+      m = mn;
+    }
+    if (tl && tid == 0) tl[6] = clock_now();
+    // The denominator of each head over the wave's slots: its four lane groups.
+    ls += lane_xor<16>(ls, lane);
+    ls += lane_xor<32>(ls, lane);
+    const int h = lane & 15;
+    if (h < G) {
+      float* w = wst + (wave * GT + h) * (D + 2);
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) w[16 * db + 4 * (lane >> 4) + r] = o[db][r];
+      if ((lane >> 4) == 0) { w[D] = m; w[D + 1] = ls; }
+    }
+  } else {
+    float qr[GT][8];
+  #pragma unroll
+    for (int h = 0; h < GT; ++h)
+  #pragma unroll
+      for (int e = 0; e < 8; ++e) qr[h][e] = (h < G) ? qs[h * D + de + e] * p.q_scale : 0.f;
+    float m[GT], ls[GT], acc[GT][8];
+  #pragma unroll
+    for (int h = 0; h < GT; ++h) {
+      m[h] = -INFINITY; ls[h] = 0.f;
+  #pragma unroll
+      for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+    }
+    // One block of NB slot passes (all wave-uniform): the scores of every slot in the block
+    // first, then one running maximum per head shared by the whole wave, then the exponentials
+    // and the weighted V sums. Because the maximum is the same in every lane, the wave's slot
+    // groups are combined at the end by plain sums, with no rescaling. ok[s] says the wave holds
+    // pass s; val[s] that this lane's slot in it is live. refill_k / refill_v(s) are called once
+    // pass s's K (V) registers are no longer needed.
+    auto block = [&](auto nbc, const u32x4* kw, const u32x4* vw, const bool* ok, const bool* val, auto refill_k,
+                     auto refill_v) {
+      constexpr int NB = decltype(nbc)::value;
+      float sc[NB][GT];
+  #pragma unroll
+      for (int s = 0; s < NB; ++s) {
+  #pragma unroll
+        for (int h = 0; h < GT; ++h) sc[s][h] = -INFINITY;
+        if (ok[s]) {
+          const u32x4 k = kw[s];
+          const float kf[8] = {bf16lo(k.x), bf16hi(k.x), bf16lo(k.y), bf16hi(k.y),
+                               bf16lo(k.z), bf16hi(k.z), bf16lo(k.w), bf16hi(k.w)};
+          refill_k(s);
+  #pragma unroll
+          for (int h = 0; h < GT; ++h) {
+            if (h < G) {
+              float x = 0.f;
+  #pragma unroll
+              for (int e = 0; e < 8; ++e) x = fmaf(qr[h][e], kf[e], x);
+              x = (LPS == 16) ? row16_sum(x) : row8_sum(x);
+              sc[s][h] = val[s] ? x : -INFINITY;
+            }
           }
         }
       }
-    }
-#pragma unroll
-    for (int h = 0; h < GT; ++h) {
-      float bm = sc[0][h];
-#pragma unroll
-      for (int s = 1; s < NB; ++s) bm = fmaxf(bm, sc[s][h]);
-      bm = max_slot_groups<LPS>(bm, lane);
-      const float mn = fmaxf(m[h], bm);
-      const float a = (m[h] == -INFINITY) ? 0.f : exp2f(m[h] - mn);
-      ls[h] *= a;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[h][e] *= a;
-      m[h] = mn;
-    }
-#pragma unroll
-    for (int s = 0; s < NB; ++s) {
-      if (ok[s]) {
-        const u32x4 v = vw[s];
-        const float vf[8] = {bf16lo(v.x), bf16hi(v.x), bf16lo(v.y), bf16hi(v.y),
-                             bf16lo(v.z), bf16hi(v.z), bf16lo(v.w), bf16hi(v.w)};
-        refill_v(s);
-#pragma unroll
-        for (int h = 0; h < GT; ++h) {
-          const float pw = (sc[s][h] == -INFINITY) ? 0.f : exp2f(sc[s][h] - m[h]);
-          ls[h] += pw;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pw, vf[e], acc[h][e]);
+  #pragma unroll
+      for (int h = 0; h < GT; ++h) {
+        float bm = sc[0][h];
+  #pragma unroll
+        for (int s = 1; s < NB; ++s) bm = fmaxf(bm, sc[s][h]);
+        bm = max_slot_groups<LPS>(bm, lane);
+        const float mn = fmaxf(m[h], bm);
+        const float a = (m[h] == -INFINITY) ? 0.f : exp2f(m[h] - mn);
+        ls[h] *= a;
+  #pragma unroll
+        for (int e = 0; e < 8; ++e) acc[h][e] *= a;
+        m[h] = mn;
+      }
+  #pragma unroll
+      for (int s = 0; s < NB; ++s) {
+        if (ok[s]) {
+          const u32x4 v = vw[s];
+          const float vf[8] = {bf16lo(v.x), bf16hi(v.x), bf16lo(v.y), bf16hi(v.y),
+                               bf16lo(v.z), bf16hi(v.z), bf16lo(v.w), bf16hi(v.w)};
+          refill_v(s);
+  #pragma unroll
+          for (int h = 0; h < GT; ++h) {
+            const float pw = (sc[s][h] == -INFINITY) ? 0.f : exp2f(sc[s][h] - m[h]);
+            ls[h] += pw;
+  #pragma unroll
+            for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pw, vf[e], acc[h][e]);
+          }
         }
       }
+    };
+    if (tl && tid == 0) tl[2] = clock_now();
+    const int n_arena = t_end - t0;
+    const int npass = n_arena > 0 ? (n_arena + SPP - 1) / SPP : 0;
+    for (int pb = 0; pb < npass; pb += NPF) {
+      bool ok[NPF], val[NPF];
+  #pragma unroll
+      for (int sl = 0; sl < NPF; ++sl) {
+        const int pass = pb + sl;
+        ok[sl] = pass < npass;
+        val[sl] = t0 + pass * SPP + wave * SPW + ssl < t_end;
+      }
+      block(std::integral_constant<int, NPF>{}, kr, vr, ok, val,
+            [&](int sl) { issue_k(sl, pb + sl + NPF); }, [&](int sl) { issue_v(sl, pb + sl + NPF); });
     }
-  };
-  if (tl && tid == 0) tl[2] = clock_now();
-  const int n_arena = t_end - t0;
-  const int npass = n_arena > 0 ? (n_arena + SPP - 1) / SPP : 0;
-  for (int pb = 0; pb < npass; pb += NPF) {
-    bool ok[NPF], val[NPF];
-#pragma unroll
-    for (int sl = 0; sl < NPF; ++sl) {
-      const int pass = pb + sl;
-      ok[sl] = pass < npass;
-      val[sl] = t0 + pass * SPP + wave * SPW + ssl < t_end;
+    if (is_last && wave == 0) {
+      // The new slot, as stored (bf16), in the first slot group of wave 0.
+      u32x4 kw1, vw1;
+      u32 kp[4], vp[4];
+  #pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        kp[j] = (__float_as_uint(ks[de + 2 * j]) >> 16) | (__float_as_uint(ks[de + 2 * j + 1]) & 0xffff0000u);
+        vp[j] = (__float_as_uint(vs[de + 2 * j]) >> 16) | (__float_as_uint(vs[de + 2 * j + 1]) & 0xffff0000u);
+      }
+      kw1 = u32x4{kp[0], kp[1], kp[2], kp[3]};
+      vw1 = u32x4{vp[0], vp[1], vp[2], vp[3]};
+      const bool ok1[1] = {true}, val1[1] = {ssl == 0};
+      block(std::integral_constant<int, 1>{}, &kw1, &vw1, ok1, val1, [](int) {}, [](int) {});
     }
-    block(std::integral_constant<int, NPF>{}, kr, vr, ok, val,
-          [&](int sl) { issue_k(sl, pb + sl + NPF); }, [&](int sl) { issue_v(sl, pb + sl + NPF); });
-  }
-  if (is_last && wave == 0) {
-    // The new slot, as stored (bf16), in the first slot group of wave 0.
-    u32x4 kw1, vw1;
-    u32 kp[4], vp[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      kp[j] = (__float_as_uint(ks[de + 2 * j]) >> 16) | (__float_as_uint(ks[de + 2 * j + 1]) & 0xffff0000u);
-      vp[j] = (__float_as_uint(vs[de + 2 * j]) >> 16) | (__float_as_uint(vs[de + 2 * j + 1]) & 0xffff0000u);
-    }
-    kw1 = u32x4{kp[0], kp[1], kp[2], kp[3]};
-    vw1 = u32x4{vp[0], vp[1], vp[2], vp[3]};
-    const bool ok1[1] = {true}, val1[1] = {ssl == 0};
-    block(std::integral_constant<int, 1>{}, &kw1, &vw1, ok1, val1, [](int) {}, [](int) {});
-  }
-  if (tl && tid == 0) tl[6] = clock_now();
-  sum_slot_groups<LPS, GT>(ls, acc);
-  if (ssl == 0) {
-#pragma unroll
-    for (int h = 0; h < GT; ++h) {
-      if (h < G) {
-        float* w = wst + (wave * GT + h) * (D + 2);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) w[de + e] = acc[h][e];
-        if (de == 0) { w[D] = m[h]; w[D + 1] = ls[h]; }
+    if (tl && tid == 0) tl[6] = clock_now();
+    sum_slot_groups<LPS, GT>(ls, acc);
+    if (ssl == 0) {
+  #pragma unroll
+      for (int h = 0; h < GT; ++h) {
+        if (h < G) {
+          float* w = wst + (wave * GT + h) * (D + 2);
+  #pragma unroll
+          for (int e = 0; e < 8; ++e) w[de + e] = acc[h][e];
+          if (de == 0) { w[D] = m[h]; w[D + 1] = ls[h]; }
+        }
       }
     }
   }
