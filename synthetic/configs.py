@@ -60,6 +60,10 @@ CONFIGS = {
                         batch=4, ctx=(1, 900), steps=3),
     "mini-llama2-b8": _c(k=15, n_layers=2, hidden=1280, n_heads=10, n_kv_heads=10, head_dim=128,
                          intermediate=3456, vocab=3001, batch=8, ctx=(3, 700), steps=3),
+    # head_dim 64 with three query heads per KV head (a padded head group on the matrix-core
+    # attention path) and four ragged lanes (matrix-core GEMV tiles)
+    "mini-gqa3-b4": _c(k=17, n_layers=2, hidden=768, n_heads=12, n_kv_heads=4, head_dim=64,
+                       intermediate=2048, vocab=3011, rope_theta=5e5, batch=4, ctx=(1, 600), steps=3),
 }
 
 

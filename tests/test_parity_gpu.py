@@ -31,6 +31,7 @@ def _need_gpu():
     ("mini-llama2", "ones"),
     ("mini-qwen3-b4", "uniform"),
     ("mini-llama2-b8", "ones"),
+    ("mini-gqa3-b4", "uniform"),
 ])
 def test_megakernel_matches_oracle(name, gains):
     from tests.gpu_harness import Pair
