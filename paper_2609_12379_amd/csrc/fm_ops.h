@@ -260,6 +260,9 @@ __device__ __forceinline__ void cursor_next(GemvCursor& c, const GemvGeom& g, in
 // or the slab's segments, rows past the tile, the ragged last segment) read their slot of
 // the zero page, which stays in cache.
 // Unit shape: 4 rows x 128 columns (VALU tiles) or 16 rows x 32 columns (matrix-core tiles).
+// Padding of each matrix-core activation plane row, in bf16 values (16 bytes).
+constexpr int XPAD = 8;
+
 template <bool MF> struct UnitShape {
   static constexpr int rows = MF ? 16 : 4, cols = MF ? 32 : 128;
   __device__ static int row(int lane) { return MF ? (lane & 15) : (lane >> 4); }
@@ -348,8 +351,9 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
   constexpr int XSF = xslab_floats<B>();
   {
     const int Kpad = (K + 127) & ~127;
-    // fp32 slab [B][Ks], or three bf16 planes [3][B][Ks] (6 bytes per value) on the matrix cores
-    const int ks = (MF ? (XSF * 4) / (6 * B) : XSF / B) & ~127;
+    // fp32 slab [B][Ks], or three bf16 planes [3][B][Ks + XPAD] (6 bytes per value) on the
+    // matrix cores
+    const int ks = (MF ? (XSF * 4) / (6 * B) - XPAD : XSF / B) & ~127;
     g.Ks = ks < Kpad ? ks : Kpad;
   }
   g.K = uni(K);
@@ -417,7 +421,11 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
   const bool ctl = (NCTL == 0) || wave >= NSW;
   const int ct = NCTL ? tid - NSW * 64 : tid, nct = NCTL ? NCTL * 64 : NT;
   uint16_t* planes = reinterpret_cast<uint16_t*>(xs);   // matrix-core tiles: [3][B][Ks]
-  const int pst = B * g.Ks;                             // values per plane
+  // Matrix-core planes: rows of Ks + XPAD values, so the batch rows that one 8-lane group reads
+  // for a B operand (same columns, consecutive rows) start 16 bytes apart and fall in
+  // different LDS banks (with rows of Ks values, a multiple of 128, they all shared banks).
+  const int RS = MF ? g.Ks + XPAD : g.Ks;                // values per plane row
+  const int pst = B * RS;                               // values per plane
   auto put_pair = [&](int i, int k, float a, float b) {
     if constexpr (MF) {
       const uint16_t h0 = to_bf16(a), h1 = to_bf16(b);
@@ -427,7 +435,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
       a -= __uint_as_float((u32)m0_ << 16);
       b -= __uint_as_float((u32)m1_ << 16);
       const uint16_t l0 = to_bf16(a), l1 = to_bf16(b);
-      u32* q = reinterpret_cast<u32*>(planes + i * g.Ks + k);
+      u32* q = reinterpret_cast<u32*>(planes + i * RS + k);
       q[0] = (u32)h0 | ((u32)h1 << 16);
       q[pst / 2] = (u32)m0_ | ((u32)m1_ << 16);
       q[pst] = (u32)l0 | ((u32)l1 << 16);
@@ -530,7 +538,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
           const int kk = seg * 32 + (lane >> 4) * 8;      // this lane's 8-column block
           bf16x8 xh = {}, xm = {}, xl = {};
           if (j < B) {
-            const uint16_t* pl = planes + j * g.Ks + kk;
+            const uint16_t* pl = planes + j * RS + kk;
             xh = *reinterpret_cast<const bf16x8*>(pl);
             xm = *reinterpret_cast<const bf16x8*>(pl + pst);
             xl = *reinterpret_cast<const bf16x8*>(pl + 2 * pst);
