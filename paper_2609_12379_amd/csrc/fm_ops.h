@@ -755,20 +755,21 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
 
 // Chunk length of this step (see above); spp is the pass width.
 // gran (<= spp) is the work granularity of one wave: chunks shorter than half a pass are
-// rounded to it instead (short contexts then keep many items, each on a few waves).
-__device__ __forceinline__ int chunk_len(CParams& p, const Step& st, int spp, int gran) {
+// rounded to it instead (short contexts then keep many items, each on a few waves). tmin is
+// the shortest chunk worth its share of the merge.
+__device__ __forceinline__ int chunk_len(CParams& p, const Step& st, int spp, int gran, int tmin) {
   long long total = 0;
   for (int ii = 0; ii < p.b; ++ii) total += st.kvl[ii] + 1;
   total *= p.nkv;
   const long long denom = p.P - p.nkv * p.b;
   const int T0 = (int)((total + denom - 1) / denom);
   const int q = (2 * T0 <= spp) ? gran : spp;
-  return ((T0 + q - 1) / q) * q;
+  return max(((T0 + q - 1) / q) * q, tmin);
 }
 
-__device__ __forceinline__ bool item_map(CParams& p, const Step& st, int j, int spp, int gran, int& i, int& g,
-                                         int& c, int& nc, int& t0, int& t1) {
-  const int T = chunk_len(p, st, spp, gran);
+__device__ __forceinline__ bool item_map(CParams& p, const Step& st, int j, int spp, int gran, int tmin, int& i,
+                                         int& g, int& c, int& nc, int& t0, int& t1) {
+  const int T = chunk_len(p, st, spp, gran, tmin);
   int idx = j;
   for (int ii = 0; ii < p.b; ++ii) {
     const int W = st.kvl[ii] + 1;
@@ -917,7 +918,9 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
   constexpr int KB = D / 32, DB = D / 16;   // 32-dim blocks (scores), 16-dim blocks (V sums)
   const int l = uni(ins[1]), j = uni(ins[2]);
   int i, g, c, nc, t0, t1;
-  if (!item_map(p, st, j, SPP, MFA ? 16 : SPP, i, g, c, nc, t0, t1)) return true;
+  // VALU items cover at least 64 slots (two passes at d = 128): shorter chunks cost the merger
+  // more than they save (measured on the Qwen3-0.6B shape at context 512).
+  if (!item_map(p, st, j, SPP, MFA ? 16 : SPP, MFA ? 16 : 64, i, g, c, nc, t0, t1)) return true;
   i = uni(i); g = uni(g); c = uni(c); nc = uni(nc); t0 = uni(t0); t1 = uni(t1);
   const int G = p.G;
   const int kvl = uni(st.kvl[i]);
