@@ -910,10 +910,11 @@ template <int D, int GT>
 __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_t* ins, float* smem, int tid,
                                         int lane, int wave, u64* tl) {
   // Grouped-query kernels with d = 64 (GT >= 2) run the scores and the weighted V sums on the
-  // matrix cores in tiles of 16 slots per wave (pass width 128). The transposed V operand costs
-  // four 2-byte loads per 16 dims; at d = 128 that outweighed the gain (measured), so those
+  // matrix cores in tiles of 16 slots per wave (pass width 128). At d = 128 the matrix-core
+  // tiles measured slower on the Qwen3-0.6B shape and barely faster elsewhere, so those
   // kernels, and one-head-per-group kernels, use the VALU.
   constexpr bool MFA = GT >= 2 && D == 64;
+  constexpr int VROW = D + 4;               // LDS row of one V slot, in bf16 values
   constexpr int LPS = D / 8, SPW = 64 / LPS, SPP = MFA ? 16 * NWAVE : SPW * NWAVE, NPF = 4;
   constexpr int KB = D / 32, DB = D / 16;   // 32-dim blocks (scores), 16-dim blocks (V sums)
   const int l = uni(ins[1]), j = uni(ins[2]);
@@ -944,36 +945,23 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
   auto issue_k = [&](int slot, int pass) { kr[slot] = __builtin_amdgcn_raw_buffer_load_b128(rk, kv_off(pass), 0, CPOL_NT); };
   auto issue_v = [&](int slot, int pass) { vr[slot] = __builtin_amdgcn_raw_buffer_load_b128(rv, kv_off(pass), 0, CPOL_NT); };
   // Matrix-core tiles: 16 slots s0 .. s0 + 15. K in the A-operand layout of the score product
-  // (lane l: slot s0 + l % 16, dims 32 kb + 8 (l / 16) .. + 8: one 16-byte load per block);
-  // V transposed, in the A-operand layout of the V sums (lane l: dim 16 db + l % 16 of slots
-  // s0 + 4 (l / 16) .. + 4: four 2-byte loads per block, packed two to a register). Slots past
-  // the chunk load zeros (out-of-range offsets).
+  // (lane l: slot s0 + l % 16, dims 32 kb + 8 (l / 16) .. + 8: one 16-byte load per block); V
+  // rows loaded the same way, to be transposed through LDS. Slots past the chunk load zeros
+  // (out-of-range offsets).
   u32x4 kA[MFA ? KB : 1], kB2[MFA ? KB : 1];
-  u32 vA[MFA ? DB : 1][2], vB2[MFA ? DB : 1][2];
-  auto tile_load = [&](u32x4* kt, u32 (*vt)[2], int s0) {
+  u32x4 wA[MFA ? KB : 1], wB2[MFA ? KB : 1];
+  auto tile_load = [&](u32x4* kt, u32x4* wt, int s0) {
     const int tk = s0 + (lane & 15);
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
-      kt[kb] = __builtin_amdgcn_raw_buffer_load_b128(
-          rk, tk < t_end ? ((head_slot0 + (u32)tk) * (u32)D + (u32)(32 * kb + 8 * (lane >> 4))) * 2u : 0xFFFFFFF0u, 0,
-          CPOL_NT);
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      u32 h[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int tv = s0 + 4 * (lane >> 4) + r;
-        h[r] = __builtin_amdgcn_raw_buffer_load_b16(
-            rv, tv < t_end ? ((head_slot0 + (u32)tv) * (u32)D + (u32)(16 * db + (lane & 15))) * 2u : 0xFFFFFFF0u, 0,
-            CPOL_NT);
-      }
-      vt[db][0] = h[0] | (h[1] << 16);
-      vt[db][1] = h[2] | (h[3] << 16);
+    for (int kb = 0; kb < KB; ++kb) {
+      const u32 off = tk < t_end ? ((head_slot0 + (u32)tk) * (u32)D + (u32)(32 * kb + 8 * (lane >> 4))) * 2u : 0xFFFFFFF0u;
+      kt[kb] = __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, CPOL_NT);
+      wt[kb] = __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, CPOL_NT);
     }
   };
   if constexpr (MFA) {
-    tile_load(kA, vA, t0 + 16 * wave);
-    tile_load(kB2, vB2, t0 + 16 * (wave + NWAVE));
+    tile_load(kA, wA, t0 + 16 * wave);
+    tile_load(kB2, wB2, t0 + 16 * (wave + NWAVE));
   } else {
 #pragma unroll
     for (int s = 0; s < NPF; ++s) { issue_k(s, s); issue_v(s, s); }
@@ -997,6 +985,7 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
   // LDS: the merger's partials at the start, this item's working vectors near the end.
   static_assert(GT * D + 2 * D + NWAVE * GT * (D + 2) <= ATT_FLOATS, "attention LDS");
   static_assert(kMergeFloats + 3 * KB * 64 * 4 <= LDS_FLOATS - MISC_FLOATS - ATT_FLOATS, "q planes in LDS");
+  static_assert(NWAVE * 16 * VROW <= 2 * kMergeFloats, "V tiles in the merge region");
   float* cp = smem;                 // [G][nc][D + 2], at most kMergeFloats
   float* qs = smem + LDS_FLOATS - MISC_FLOATS - ATT_FLOATS;  // [G][D]
   float* ks = qs + GT * D;          // [D]
@@ -1091,7 +1080,18 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
     // operand (slots 4 (l / 16) .. + 4 of head l % 16) is the score tile's own C layout. P is
     // split into three bf16 planes like q.
     typedef short s16x4 __attribute__((ext_vector_type(4)));
-    auto tile = [&](const u32x4* kt, const u32 (*vt)[2], auto live_row) {
+    uint16_t* vbuf = reinterpret_cast<uint16_t*>(smem) + wave * 16 * VROW;   // this wave's V tile
+    auto tile = [&](const u32x4* kt, const u32x4* wt, auto live_row) {
+      // V rows into LDS ([16 slots][VROW]; rows 8 bytes longer than d so that the four slot
+      // rows read together below fall in different banks), read back transposed below.
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        u32* dst = reinterpret_cast<u32*>(vbuf + (lane & 15) * VROW + 32 * kb + 8 * (lane >> 4));
+        dst[0] = wt[kb].x; dst[1] = wt[kb].y; dst[2] = wt[kb].z; dst[3] = wt[kb].w;
+      }
+      // The rows are written as 32-bit words and read back as 16-bit values: keep the compiler
+      // from moving the reads above the writes (type-based alias analysis would).
+      asm volatile("" ::: "memory");
       f32x4 sc4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
@@ -1128,12 +1128,15 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
       }
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const s16x4 va = {(short)(vt[db][0] & 0xffffu), (short)(vt[db][0] >> 16), (short)(vt[db][1] & 0xffffu),
-                          (short)(vt[db][1] >> 16)};
+        // V^T operand: dim 16 db + l % 16 of slots 4 (l / 16) .. + 4.
+        s16x4 va;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) va[r] = (short)vbuf[(4 * (lane >> 4) + r) * VROW + 16 * db + (lane & 15)];
         o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pl, o[db], 0, 0, 0);
         o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pm, o[db], 0, 0, 0);
         o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, ph, o[db], 0, 0, 0);
       }
+      asm volatile("" ::: "memory");   // the next tile's rows are written after these reads
     };
     if (tl && tid == 0) tl[2] = clock_now();
     // This wave's tiles: 16-slot tiles wave, wave + 8, ... of the chunk, two in flight.
@@ -1142,13 +1145,13 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
     for (int k = 0; k < ntile; k += 2) {
       {
         const int s0 = t0 + 16 * (wave + NWAVE * k);
-        tile(kA, vA, [&](int r) { return s0 + 4 * (lane >> 4) + r < t_end; });
-        if (k + 2 < ntile) tile_load(kA, vA, t0 + 16 * (wave + NWAVE * (k + 2)));
+        tile(kA, wA, [&](int r) { return s0 + 4 * (lane >> 4) + r < t_end; });
+        if (k + 2 < ntile) tile_load(kA, wA, t0 + 16 * (wave + NWAVE * (k + 2)));
       }
       if (k + 1 < ntile) {
         const int s0 = t0 + 16 * (wave + NWAVE * (k + 1));
-        tile(kB2, vB2, [&](int r) { return s0 + 4 * (lane >> 4) + r < t_end; });
-        if (k + 3 < ntile) tile_load(kB2, vB2, t0 + 16 * (wave + NWAVE * (k + 3)));
+        tile(kB2, wB2, [&](int r) { return s0 + 4 * (lane >> 4) + r < t_end; });
+        if (k + 3 < ntile) tile_load(kB2, wB2, t0 + 16 * (wave + NWAVE * (k + 3)));
       }
     }
     if (is_last && wave == 0) {
