@@ -146,12 +146,6 @@ __device__ __forceinline__ void st_tag(u64* p, float v, u32 epoch) {
   __hip_atomic_store(p, tag(v, epoch), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
 // Sum within each 16-lane row; every lane of the row gets the total (DPP, no LDS).
 __device__ __forceinline__ float row16_sum(float s) {
   s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0xB1, 0xF, 0xF, false));   // quad [1,0,3,2]
@@ -159,6 +153,47 @@ __device__ __forceinline__ float row16_sum(float s) {
   s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x141, 0xF, 0xF, false));  // half-row mirror
   s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x140, 0xF, 0xF, false));  // row mirror
   return s;
+}
+
+// Value of lane (lane xor 16) / (lane xor 32), on the VALU. permlane16_swap(a, a): the first
+// result holds row r & ~1 in both rows of a pair, the second row r | 1; permlane32_swap(a, a):
+// the first result holds lanes 0-31 in both halves, the second 32-63.
+__device__ __forceinline__ u32 xor16_u32(u32 v, int lane) {
+  auto p = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return ((lane >> 4) & 1) ? p[0] : p[1];
+}
+__device__ __forceinline__ u32 xor32_u32(u32 v, int lane) {
+  auto p = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return (lane >> 5) ? p[0] : p[1];
+}
+
+// Sum over the wave; every lane gets the same total. VALU only (DPP within rows, permlane
+// swaps across them): cross-lane shuffles through the LDS crossbar cost about 100 cycles per
+// dependent step.
+__device__ __forceinline__ float wave_sum(float v) {
+  const int lane = __lane_id();
+  v = row16_sum(v);
+  v += __uint_as_float(xor16_u32(__float_as_uint(v), lane));
+  v += __uint_as_float(xor32_u32(__float_as_uint(v), lane));
+  return v;
+}
+
+// Maximum of a 64-bit key over the wave (same exchanges as wave_sum).
+__device__ __forceinline__ u64 wave_max_u64(u64 k) {
+  const int lane = __lane_id();
+  auto take = [&](u32 lo, u32 hi) {
+    const u64 o = ((u64)hi << 32) | lo;
+    k = o > k ? o : k;
+  };
+#define FM_DPP_U32(v, ctl) ((u32)__builtin_amdgcn_mov_dpp((int)(v), ctl, 0xF, 0xF, false))
+  take(FM_DPP_U32(k, 0xB1), FM_DPP_U32(k >> 32, 0xB1));
+  take(FM_DPP_U32(k, 0x4E), FM_DPP_U32(k >> 32, 0x4E));
+  take(FM_DPP_U32(k, 0x141), FM_DPP_U32(k >> 32, 0x141));
+  take(FM_DPP_U32(k, 0x140), FM_DPP_U32(k >> 32, 0x140));
+#undef FM_DPP_U32
+  take(xor16_u32((u32)k, lane), xor16_u32((u32)(k >> 32), lane));
+  take(xor32_u32((u32)k, lane), xor32_u32((u32)(k >> 32), lane));
+  return k;
 }
 
 __device__ __forceinline__ u64 clock_now() { return wall_clock64(); }

@@ -696,14 +696,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
     u64* wkeys = reinterpret_cast<u64*>(misc + 16);   // [NWAVE][B]
 #pragma unroll
     for (int i = 0; i < B; ++i) {
-      u64 k = key[i];
-#pragma unroll
-      for (int o = 32; o >= 1; o >>= 1) {
-        const u32 lo = __shfl_xor((u32)(k & 0xFFFFFFFFull), o, 64);
-        const u32 hi = __shfl_xor((u32)(k >> 32), o, 64);
-        const u64 ko = ((u64)hi << 32) | lo;
-        k = ko > k ? ko : k;
-      }
+      const u64 k = wave_max_u64(key[i]);
       if (lane == 0) wkeys[wave * B + i] = k;
     }
     __syncthreads();
@@ -797,17 +790,8 @@ __device__ __forceinline__ float row8_sum(float s) {
 __device__ __forceinline__ float lane_xor8(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xF, 0xF, false));  // row rotate 8
 }
-__device__ __forceinline__ float lane_xor16(float v, int lane) {
-  // permlane16_swap(a, a): the first result holds row r & ~1 in both rows of a pair, the
-  // second row r | 1.
-  auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(((lane >> 4) & 1) ? p[0] : p[1]);
-}
-__device__ __forceinline__ float lane_xor32(float v, int lane) {
-  // permlane32_swap(a, a): the first result holds lanes 0-31 in both halves, the second 32-63.
-  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float((lane >> 5) ? p[0] : p[1]);
-}
+__device__ __forceinline__ float lane_xor16(float v, int lane) { return __uint_as_float(xor16_u32(__float_as_uint(v), lane)); }
+__device__ __forceinline__ float lane_xor32(float v, int lane) { return __uint_as_float(xor32_u32(__float_as_uint(v), lane)); }
 template <int O>
 __device__ __forceinline__ float lane_xor(float v, int lane) {
   static_assert(O == 8 || O == 16 || O == 32, "exchange distance");
@@ -1159,11 +1143,12 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
       // score for each head (a wave sum over the dims), then the usual update of this lane's
       // head. The denominator counts it once, in the first lane group.
       float s_new = -INFINITY;
-      for (int hh = 0; hh < G; ++hh) {
-        float x = qs[hh * D + lane] * p.q_scale * ks[lane];
-        if (D > 64) x = fmaf(qs[hh * D + lane + 64] * p.q_scale, ks[lane + 64], x);
+#pragma unroll
+      for (int hh = 0; hh < GT; ++hh) {   // unrolled: the heads' reductions interleave
+        float x = hh < G ? qs[hh * D + lane] * p.q_scale * ks[lane] : 0.f;
+        if (D > 64 && hh < G) x = fmaf(qs[hh * D + lane + 64] * p.q_scale, ks[lane + 64], x);
         x = wave_sum(x);
-        if ((lane & 15) == hh) s_new = x;
+        if ((lane & 15) == hh && hh < G) s_new = x;
       }
       const float mn = fmaxf(m, s_new);
       const float a = (m == -INFINITY) ? 0.f : exp2f(m - mn);
