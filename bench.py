@@ -71,6 +71,8 @@ def main():
                     help="also run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--nwg", type=int, default=0)
     ap.add_argument("--attn-items", type=int, default=0)
+    ap.add_argument("--context", type=int, default=0,
+                    help="prefilled context of every lane, overriding the workload's (a context sweep)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -87,6 +89,8 @@ def main():
     load()  # fail loudly if the HIP library is missing
     assert torch.cuda.is_available(), "bench.py needs the GPU"
     cfg0 = get_config(args.config)
+    if args.context:
+        cfg0 = dict(cfg0, ctx=(args.context, args.context))
     total_steps = args.warmup + args.steps
     t_gen = time.time()
     # weights and KV prefill are drawn on the device (seeded, same distributions as the host recipe)
@@ -178,7 +182,7 @@ def main():
                      "frac": round(achieved_gbs / PEAK_GBS, 4), "traffic": None,
                      "kernel": "fm::dev::step_kernel (one launch per step)"},
     }
-    tr = profiled_traffic(cfg["name"])
+    tr = None if args.context else profiled_traffic(cfg["name"])
     if tr is not None:
         out["roofline"]["traffic"] = tr["traffic_bytes_per_launch"]
         out["read_amplification_rho"] = round(tr["fetch_bytes_per_launch"] / mean_bytes, 4)
