@@ -148,6 +148,27 @@ fm_status fm_decode_step_multilaunch(fm_handle *h, const int32_t *token_ids,
                                      const int32_t *positions, const int32_t *kv_lens,
                                      float *logits_out, int32_t *next_ids, hipStream_t stream);
 
+/* Prompt extension (prefill) as a loop of single-token steps, the way the paper's serving
+ * integration runs an extend batch (Sec. 4.3, deployment in a serving engine): n_tokens
+ * decode steps of all b lanes, launched back to back on `stream` with no host
+ * synchronisation between them. Step t reads row t of each array:
+ *   token_ids   device int32[n_tokens][b]: the prompt token of lane i at step t
+ *               (teacher-forced: the steps never feed back their own greedy tokens);
+ *   positions   device int32[n_tokens][b]: its RoPE position;
+ *   kv_lens     device int32[n_tokens][b]: its cache slot, as for fm_decode_step. A lane
+ *               normally uses kv_lens = positions = its cached length + t. A lane whose
+ *               prompt is shorter than n_tokens repeats its last row, which recomputes
+ *               the same slot.
+ *   logits_out  device fp32 [b][vocab], written by the last step only (NULL: not written);
+ *   next_ids    device int32[b]: the greedy tokens of the last step (the first generated
+ *               tokens). Every step writes it, so it must not alias token_ids.
+ * Each step is exactly fm_decode_step: the results are bit-identical to n_tokens such calls.
+ * n_tokens = 0 does nothing. Errors are those of fm_decode_step. The first failing step's
+ * status is returned and later steps are not launched. */
+fm_status fm_extend(fm_handle *h, const int32_t *token_ids, const int32_t *positions,
+                    const int32_t *kv_lens, int32_t n_tokens, float *logits_out, int32_t *next_ids,
+                    hipStream_t stream);
+
 /* Release the handle's scratch. The caller's buffers are untouched. */
 fm_status fm_destroy(fm_handle *h);
 

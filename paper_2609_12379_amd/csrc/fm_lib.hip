@@ -306,6 +306,19 @@ fm_status fm_decode_step_multilaunch(fm_handle* h, const int32_t* token_ids, con
   return launch(h, token_ids, positions, kv_lens, logits_out, next_ids, stream, true);
 }
 
+fm_status fm_extend(fm_handle* h, const int32_t* token_ids, const int32_t* positions, const int32_t* kv_lens,
+                    int32_t n_tokens, float* logits_out, int32_t* next_ids, hipStream_t stream) {
+  if (!h || !token_ids || !positions || !kv_lens || !next_ids || n_tokens < 0) return FM_ERR_INVALID_ARG;
+  const size_t b = (size_t)h->base.b;
+  for (int32_t t = 0; t < n_tokens; ++t) {
+    const size_t r = (size_t)t * b;
+    const fm_status s = launch(h, token_ids + r, positions + r, kv_lens + r,
+                               t + 1 == n_tokens ? logits_out : nullptr, next_ids, stream, false);
+    if (s != FM_OK) return s;
+  }
+  return FM_OK;
+}
+
 fm_status fm_destroy(fm_handle* h) {
   if (!h) return FM_ERR_INVALID_ARG;
   hipDeviceSynchronize();

@@ -46,7 +46,7 @@ class fm_plan_stats(ctypes.Structure):
         ("imbalance", ctypes.c_double)]
 
 
-EXPORTS = ("fm_create", "fm_decode_step", "fm_decode_step_multilaunch", "fm_destroy", "fm_last_error",
+EXPORTS = ("fm_create", "fm_decode_step", "fm_decode_step_multilaunch", "fm_extend", "fm_destroy", "fm_last_error",
            "fm_set_taps", "fm_tap_count", "fm_set_timeline", "fm_instruction_count", "fm_plan_query",
            "fm_plan_export", "fm_status_string")
 
@@ -66,6 +66,7 @@ def load():
                             ctypes.POINTER(fm_kv_ptrs), ctypes.POINTER(P)]
     for n in ("fm_decode_step", "fm_decode_step_multilaunch"):
         getattr(L, n).argtypes = [P, P, P, P, P, P, P]
+    L.fm_extend.argtypes = [P, P, P, P, I32, P, P, P]
     L.fm_destroy.argtypes = [P]
     L.fm_last_error.argtypes = [P, ctypes.POINTER(I32)]
     L.fm_set_taps.argtypes = [P, P]
@@ -178,6 +179,22 @@ class Decoder:
         st = fn(self.h, token_ids.data_ptr(), positions.data_ptr(), kv_lens.data_ptr(),
                 logits_out.data_ptr() if logits_out is not None else None, next_ids.data_ptr(), stream)
         check(st, "fm_decode_step")
+
+    def extend(self, token_ids, positions, kv_lens, logits_out, next_ids, stream=None):
+        """Prompt extension as single-token steps: token_ids, positions and kv_lens are CUDA
+        int32 tensors [n_tokens][b] (row t feeds step t); logits_out ([b][vocab] or None) and
+        next_ids ([b]) receive the last step's results."""
+        import torch
+        if stream is None:
+            stream = torch.cuda.current_stream().cuda_stream
+        b = self.cfg["batch"]
+        for t in (token_ids, positions, kv_lens):
+            assert t.is_cuda and t.dtype == torch.int32 and t.is_contiguous() and t.dim() == 2 and t.shape[1] == b
+        assert token_ids.shape == positions.shape == kv_lens.shape
+        st = load().fm_extend(self.h, token_ids.data_ptr(), positions.data_ptr(), kv_lens.data_ptr(),
+                              int(token_ids.shape[0]), logits_out.data_ptr() if logits_out is not None else None,
+                              next_ids.data_ptr(), stream)
+        check(st, "fm_extend")
 
     def set_taps(self, tap_buf):
         self._taps = tap_buf
