@@ -42,6 +42,20 @@ def test_megakernel_matches_oracle(name, gains):
     pr.close()
 
 
+@pytest.mark.parametrize("name", ["toy-gpu", "mini-gqa3-b4", "mini-qwen3", "mini-qwen3-b4"])
+def test_empty_cache_first_tokens(name):
+    """Every lane starts from an empty cache: the first step attends over its new token alone
+    (kv_len 0), and the arena past each cursor holds poison (N(0, 100^2) values) that must never
+    be read."""
+    from tests.gpu_harness import Pair
+    print(f"case {name} empty cache, poisoned arena", flush=True)
+    pr = Pair(name, gains="uniform", poison=True, cfg_override={"ctx": (0, 0)})
+    assert pr.wl.S == [0] * pr.cfg["batch"]
+    reps = pr.run(log=_log(name))
+    assert len(reps) == pr.wl.steps
+    pr.close()
+
+
 @pytest.mark.parametrize("name", ["toy-gpu", "mini-qwen3-b4"])
 def test_multilaunch_bit_identical_to_megakernel(name):
     from tests.gpu_harness import Pair
