@@ -1,5 +1,6 @@
 """The paper's fidelity bars (Sec. 4.2) on the HIP decode step, through the C ABI.
 
+Small shapes run all their steps; the full Qwen3-0.6B and Llama-3.2-1B shapes run two.
 Three implementations run every step from the same KV cache, along the golden's greedy
 continuation (teacher-forced):
   * K, the HIP kernel;
@@ -34,12 +35,19 @@ def _u16(t):
     return t.cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
 
 
-@pytest.mark.parametrize("name", ["mini-qwen3", "mini-gqa3-b4", "mini-llama2-b8"])
-def test_fidelity_bars(name):
+# (workload, norm gains, where the inputs are drawn): the small shapes over all their steps,
+# the full Qwen3-0.6B and Llama-3.2-1B shapes over two steps
+CASES = [("mini-qwen3", "uniform", "cpu"), ("mini-gqa3-b4", "uniform", "cpu"),
+         ("mini-llama2-b8", "uniform", "cpu"), ("qwen3-0.6b", "ones", "cuda"), ("llama3.2-1b", "ones", "cuda")]
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name,gains,device", CASES, ids=[c[0] for c in CASES])
+def test_fidelity_bars(name, gains, device):
     from oracle import fidelity as F
     from tests.gpu_harness import Pair, to_u16
     print(f"case {name}", flush=True)
-    pr = Pair(name, gains="uniform")
+    pr = Pair(name, gains=gains, steps=2 if device == "cuda" else None, device=device)
     cfg = pr.cfg
     L, b, d = cfg["n_layers"], cfg["batch"], cfg["head_dim"]
     nh, nkv = cfg["n_heads"], cfg["n_kv_heads"]
