@@ -613,7 +613,8 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
 #pragma unroll
     for (int i = 0; i < B; ++i) {
       float t = 0.f;
-      for (int w = 0; w < NWAVE; ++w) t += mss[w * B + i];
+      // only the waves that staged the input hold partial sums (all waves unless NCTL > 0)
+      for (int w = NCTL ? NSW : 0; w < NWAVE; ++w) t += mss[w * B + i];
       rs[i] = 1.0f / sqrtf(t / (float)K + p.eps);
     }
     if (st.taps && ra == 0) {
