@@ -67,18 +67,21 @@ enum {
   FM_DEV_WATCHDOG = 4       /* a dependency wait exceeded its time bound */
 };
 
-/* Model shape, batch and context bound. These stay fixed for the handle's lifetime: the
- * paper compiles one kernel per (model, b, S) cell (Sec. 5.3, context bins).
+/* Model shape, batch and context bound (the model configuration the schedule is compiled
+ * from, Sec. 4.1). These stay fixed for the handle's lifetime: the paper compiles one kernel
+ * per (model, b, S) cell (Sec. 5.3, context bins).
  * Supported: head_dim 64 or 128; hidden, n_heads*head_dim and intermediate multiples of 8;
- * n_heads a multiple of n_kv_heads with n_heads/n_kv_heads <= 8; batch 1..8. */
+ * n_heads a multiple of n_kv_heads with n_heads/n_kv_heads <= 8; batch 1..8.
+ * The last three integer fields are tuning knobs, not part of the model: leave them 0. */
 typedef struct fm_model_cfg {
   int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, intermediate, vocab;
   int32_t qk_norm;          /* 1: per-head RMSNorm on q and k before RoPE (Qwen3-shaped) */
   int32_t tied_embedding;   /* 1: the LM head is the embedding matrix */
   int32_t batch;            /* b: every step decodes exactly b lanes */
   int32_t max_ctx;          /* S_max: KV slots per lane per layer; also the RoPE table length */
+  /* Tuning (0 = automatic; the automatic values are the measured best on MI355X): */
   int32_t n_workgroups;     /* persistent workgroups; 0 = one per compute unit */
-  int32_t attn_items;       /* attention work items per layer; 0 = automatic */
+  int32_t attn_items;       /* attention work items per layer; 0 = about one per workgroup */
   int32_t reserved;         /* must be 0 */
   double rope_theta;        /* RoPE base */
   double rms_eps;           /* RMSNorm epsilon, inside the square root */
@@ -116,7 +119,10 @@ typedef struct fm_kv_ptrs {
 typedef struct fm_handle fm_handle;
 
 /* Build the per-CU instruction queues for this model and allocate the handle's scratch on
- * the current HIP device. Checks every pointer for NULL. Returns:
+ * the current HIP device. This is the schedule compiler of Sec. 4.1 (the interpreter step of
+ * the milestones: the model configuration becomes typed per-CU instruction streams), fixed
+ * for one (model, b, S_max) cell as in Sec. 5.3. Borrows the weight and KV pointers (see
+ * "Memory ownership" above). Checks every pointer for NULL. Returns:
  *   FM_ERR_UNSUPPORTED for a shape outside the supported set above;
  *   FM_ERR_CAPACITY if a matrix exceeds 2 GiB or the grid cannot be co-resident;
  *   FM_ERR_HIP if an allocation fails.
@@ -124,7 +130,10 @@ typedef struct fm_handle fm_handle;
 fm_status fm_create(const fm_model_cfg *cfg, const fm_weight_ptrs *w, const fm_kv_ptrs *kv,
                     fm_handle **out);
 
-/* One decode step for all lanes, as one kernel launch on `stream`. Arguments:
+/* One decode step for all lanes, as one kernel launch on `stream`: the decode step of
+ * Sec. 2.1 (embedding, per-layer RMSNorm, projections, RoPE, KV append, attention by Eq. 1,
+ * SwiGLU MLP, final norm, LM head, greedy token), generating one token per sequence from the
+ * weights and the KV cache. Arguments:
  *   token_ids   device int32[b]: token embedded for lane i.
  *   positions   device int32[b]: RoPE position of lane i's new token.
  *   kv_lens     device int32[b]: number of tokens already cached for lane i. The new K/V
@@ -141,9 +150,12 @@ fm_status fm_decode_step(fm_handle *h, const int32_t *token_ids, const int32_t *
 
 /* The same step split into one kernel launch per operator stage: per layer a QKV,
  * attention, O-projection, gate/up and down launch, plus one LM-head launch. Each launch
- * runs the same device code on the same per-CU queues. This is the ablation that the
- * single launch is measured against. Arguments and results are as for fm_decode_step.
- * The outputs are bit-identical to it. */
+ * runs the same device code on the same per-CU queues and keeps the fusions inside its
+ * stage (RMSNorm in the projection's staging, QK-norm, RoPE and the KV append in the
+ * attention items, the split-KV merge in each group's last item). This per-stage ablation
+ * measures what the single launch saves in launches and drains between stages (the launch
+ * and synchronisation costs of split-step engines, Sec. 1 and Sec. 5.2.3). Arguments and
+ * results are as for fm_decode_step. The outputs are bit-identical to it. */
 fm_status fm_decode_step_multilaunch(fm_handle *h, const int32_t *token_ids,
                                      const int32_t *positions, const int32_t *kv_lens,
                                      float *logits_out, int32_t *next_ids, hipStream_t stream);
@@ -169,14 +181,21 @@ fm_status fm_extend(fm_handle *h, const int32_t *token_ids, const int32_t *posit
                     const int32_t *kv_lens, int32_t n_tokens, float *logits_out, int32_t *next_ids,
                     hipStream_t stream);
 
-/* Release the handle's scratch. The caller's buffers are untouched. */
+/* Release the handle's scratch. The caller's buffers are untouched. No passage of the paper
+ * defines this call; it is resource management of the library. Synchronises the device
+ * first, so no step of this handle is still running. Returns FM_ERR_INVALID_ARG for NULL. */
 fm_status fm_destroy(fm_handle *h);
 
-/* Synchronise the device, then report the sticky device error code (FM_DEV_*). Debug only. */
+/* Synchronise the device, then report the sticky device error code (FM_DEV_*) in
+ * *device_code. Returns FM_OK when no error was recorded, FM_ERR_DEVICE when one was, and
+ * FM_ERR_HIP if the synchronisation fails. No passage of the paper defines this call: it
+ * reports the asynchronous errors described at the top of this file. Debug only. */
 fm_status fm_last_error(fm_handle *h, int32_t *device_code);
 
-/* Mid-state taps: when tap_buf (device fp32, fm_tap_count(cfg) floats) is non-NULL, each
- * step also writes per layer and lane the values below, in this order:
+/* Mid-state taps, for the mid-state test oracle of Sec. 4.2 (per-layer intermediate values
+ * compared against a reference decoder, layer by layer). When tap_buf (device fp32,
+ * fm_tap_count(cfg) floats, owned by the caller and kept alive while taps are on) is
+ * non-NULL, each step also writes per layer and lane the values below, in this order:
  *   a[h] | qkv[(nh + 2 nkv) d] | q_rot[nh d] | k_rot[nkv d] | o[nh d] | x1[h] | a2[h] | mlp[h] | x2[h]
  * Blocks are laid out [n_layers][batch]. After them comes the final normed vector [batch][h].
  * The fields:

@@ -22,11 +22,14 @@ Acceptance bars per step:
   * logits and every per-layer tap: max-abs <= 3e-2 and relative L2 <= 1e-2;
   * KV arena: every byte except slot kv_len[i] of each lane is unchanged (bit-exact). The
     slot's bf16 value must round from a value within tau * rms(row) of the reference's
-    pre-rounding value (one head row of d_h elements), with tau = 2e-3, half a bf16 ulp at the
-    row's rms. Two correct decoders that sum in different orders may land on either side of a
-    bf16 rounding boundary. The GPU's appended rows sit within 3e-4 rms of the fp64 values on
-    the full shapes;
-  * greedy ids equal, unless the reference's top-2 logit gap is below 1e-2.
+    pre-rounding value (one head row of d_h elements), with tau = 1e-3. The GPU's appended rows
+    sit within 3.3e-4 rms of the fp64 values on the full shapes, so tau keeps a 3x margin. Two
+    correct decoders that sum in different orders may land on either side of a bf16 rounding
+    boundary; such one-step flips are counted, and at most MAX_FLIP_FRAC of a step's appended
+    elements may differ from the reference's own rounding;
+  * greedy ids: each lane's id is the lowest-index maximum of the GPU's own logits row
+    (checked exactly), and it equals the reference's id unless the reference's logit at the
+    GPU's id is within 1e-2 of the reference's maximum (a near-tie; any other token fails).
 """
 from __future__ import annotations
 
@@ -40,8 +43,26 @@ from synthetic import make_workload, as_u16
 
 MAX_ABS = 3e-2
 REL_L2 = 1e-2
-TAU = 2e-3
+TAU = 1e-3
 TOP2_GAP = 1e-2
+# Fraction of a step's appended K/V elements whose bf16 value may differ from the reference's
+# own rounding of its fp64 value. The fp32 and fp64 oracle instantiations disagree on 0.2-0.5%
+# of them at the full shapes; the GPU, closer to fp64 than the fp32 oracle, stays below that.
+MAX_FLIP_FRAC = 2e-2
+
+
+def check_greedy(gpu_logits_row, gpu_id, ref_logits_row, ref_id, what=""):
+    """The greedy-id rule. Returns the reference's gap at the GPU's id when the ids differ
+    (a near-tie), else None. Raises AssertionError on a violation."""
+    g = np.asarray(gpu_logits_row)
+    own = int(np.argmax(g))            # numpy returns the first (lowest-index) maximum
+    assert int(gpu_id) == own, f"{what}: next_id {int(gpu_id)} is not the first argmax {own} of the GPU's logits"
+    if int(gpu_id) == int(ref_id):
+        return None
+    ref = np.asarray(ref_logits_row, np.float64)
+    gap = float(ref.max() - ref[int(gpu_id)])
+    assert gap < TOP2_GAP, f"{what}: token {int(gpu_id)} vs {int(ref_id)}: reference logit {gap:.3g} below its maximum"
+    return gap
 
 
 def to_dev(w: dict) -> dict:
@@ -175,11 +196,8 @@ class Pair:
                 rep["worst_tap"] = worst
             # greedy ids
             for i in range(cfg["batch"]):
-                row = r.logits[i]
-                top2 = np.partition(row, -2)[-2:]
-                gap = float(top2[1] - top2[0])
-                if nx[i] != r.next_ids[i]:
-                    assert gap < TOP2_GAP, f"step {t} lane {i}: token {nx[i]} vs {r.next_ids[i]} (gap {gap})"
+                gap = check_greedy(lg[i], nx[i], r.logits[i], r.next_ids[i], f"step {t} lane {i}")
+                if gap is not None:
                     rep.setdefault("near_ties", []).append((i, gap))
             # KV: strict slot rule and value window
             if check_kv:
@@ -208,7 +226,10 @@ class Pair:
                                 drift = max(drift, float((np.abs(gy - y) / rms).max()))
                             assert ok, f"step {t} layer {l} lane {i} {kind}: appended values outside the rounding window"
                             flips += nflip
+                n_app = 2 * cfg["n_layers"] * cfg["batch"] * nkv * d
+                assert flips <= MAX_FLIP_FRAC * n_app, f"step {t}: {flips} of {n_app} appended K/V elements flipped"
                 rep["kv_flips"] = flips
+                rep["kv_flip_frac"] = flips / n_app
                 rep["kv_drift_rms"] = drift
                 del before
             if force_kv:

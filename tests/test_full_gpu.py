@@ -21,7 +21,7 @@ import numpy as np
 import pytest
 import torch
 
-from tests.gpu_harness import Pair, rel_l2, MAX_ABS, REL_L2, TOP2_GAP
+from tests.gpu_harness import Pair, rel_l2, check_greedy, MAX_ABS, REL_L2, TOP2_GAP
 
 FULL = [("qwen3-0.6b", False), ("llama3.2-1b", False), ("llama2-7b", False), ("qwen3-8b", True),
         ("llama2-13b", True), ("qwen3-8b-b1", False), ("llama2-13b-b1", False)]
@@ -71,8 +71,11 @@ def test_bench_loop_llama3_2_1b():
             r = pair.orc.step(pair.kc_o, pair.vc_o, [int(v) for v in chosen[t]], p, p, precision="f64")
             for i in range(b):
                 if chosen[t + 1][i] != r.next_ids[i]:
-                    top2 = np.partition(r.logits[i], -2)[-2:]
-                    assert top2[1] - top2[0] < TOP2_GAP, f"step {t} lane {i}: {chosen[t + 1][i]} vs {r.next_ids[i]}"
+                    gap = float(np.max(r.logits[i]) - r.logits[i][int(chosen[t + 1][i])])
+                    assert gap < TOP2_GAP, f"step {t} lane {i}: {chosen[t + 1][i]} vs {r.next_ids[i]} (gap {gap})"
+        # the last step's id is the first argmax of the logits it wrote
+        for i in range(b):
+            check_greedy(last[i], chosen[K][i], r.logits[i], r.next_ids[i], f"last step lane {i}")
         ma, rl = float(np.abs(last - r.logits).max()), rel_l2(last, r.logits)
         print(f"[{name}] chained {K} steps, ids {chosen[:, 0].tolist()}, last logits max-abs {ma:.3g} rel-l2 {rl:.3g}",
               flush=True)

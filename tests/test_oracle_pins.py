@@ -214,8 +214,10 @@ def test_argmax_lowest_index_on_ties(oracle_lib):
 
 # ---- the whole step on the toy model ---------------------------------------------------
 
-def _toy(gains="uniform", seed=None):
+def _toy(gains="uniform", seed=None, tied=False):
     cfg = get_config("toy")
+    if tied:
+        cfg["tied_embedding"] = 1                # no separate LM head is drawn
     S = contexts(cfg)
     cfg["max_ctx"] = max(S) + 4
     w = make_weights(cfg, gains=gains, seed=seed)
@@ -239,6 +241,22 @@ def test_toy_step_matches_independent_numpy(oracle_lib):
     r32 = orc.step([a.copy() for a in kc], [a.copy() for a in vc], tok, pos, S, precision="f32")
     assert np.allclose(r32.logits, want, atol=1e-5, rtol=1e-5)
     assert list(r32.next_ids) == [int(np.argmax(row)) for row in r32.logits]
+
+
+def test_toy_tied_embedding_step_matches_independent_numpy(oracle_lib):
+    # tied models (Qwen3-0.6B, Llama-3.2-1B shapes): the LM head is the embedding matrix
+    from oracle.oracle import Oracle
+    cfg, w, kc, vc, S = _toy(tied=True)
+    assert "lm_head" not in w or w["lm_head"] is None
+    orc = Oracle(cfg, w)
+    tok, pos = make_start(cfg), list(S)
+    r64 = orc.step([a.copy() for a in kc], [a.copy() for a in vc], tok, pos, S, precision="f64", taps=True)
+    want, _, _ = brute.step(cfg, w, kc, vc, tok, pos, S)
+    assert np.allclose(r64.logits, want, rtol=1e-11, atol=1e-13)
+    # the logits are E a_f for the final normed state a_f, row by row
+    E = brute.bf(w["embed"])
+    for i in range(cfg["batch"]):
+        assert np.allclose(r64.logits[i], E @ r64.taps["final"][i], rtol=1e-12, atol=1e-14)
 
 
 def test_toy_kv_append_touches_exactly_one_slot(oracle_lib):

@@ -131,3 +131,60 @@ def test_bad_device_inputs_report_an_error_and_touch_nothing(bad, code):
         a.gpu_step(list(a.wl.start), S, S)
     assert ei.value.status == F.FM_ERR_DEVICE
     a.close()
+
+
+def test_exact_logit_tie_picks_the_lowest_index():
+    """Greedy ties (reading c9: the lowest index among equal maxima wins). Before every step two
+    LM-head rows per lane are set to the same bf16 vector, pointed along that lane's final normed
+    state so that the pair holds the step's largest logit. The two rows of a pair sit in LM tiles
+    of different workgroups on different XCDs, with the same row count, so both tiles sum their
+    dot products in the same order and the two logits are bit-identical: an exact tie that the
+    cross-workgroup argmax must break towards the lower row."""
+    from oracle.oracle import Oracle
+    from paper_2609_12379_amd import fm as F
+    from synthetic import as_u16
+    from tests.gpu_harness import Pair, to_u16, check_greedy
+    pr = Pair("toy-gpu", gains="uniform", taps=False)
+    cfg, S, b = pr.cfg, pr.wl.S, pr.cfg["batch"]
+    assert not cfg["tied_embedding"] and b == 2
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    qoff, ins = F.plan_export(cfg, n_cu)
+    tiles = []                                   # (workgroup, first row, rows) of every LM tile
+    for w in range(n_cu):
+        for q in range(qoff[w], qoff[w + 1]):
+            if ins[q, 0] == F.FM_OP_LM:
+                tiles.append((w, int(ins[q, 2]), int(ins[q, 3] - ins[q, 2])))
+    # pairs of equal-size tiles on different XCDs, far apart in the vocabulary, one pair per lane
+    nr = max(set(t[2] for t in tiles), key=lambda n: sum(t[2] == n for t in tiles))
+    same = [t for t in tiles if t[2] == nr]
+    pairs = []
+    for first in (2, 5):
+        ta = same[first]
+        tb = [t for t in same if t[0] % 8 != ta[0] % 8][-1 - first]
+        pairs.append((ta[1] + 1, tb[1] + 1))     # the same position inside each tile
+    print(f"tie pairs {pairs} in LM tiles of {nr} rows", flush=True)
+    wts = to_u16(pr.wl.weights)
+    orc = Oracle(cfg, wts)                       # holds views of wts: edits below reach it
+    lm_host = wts["lm_head"]
+    lm_dev = pr.wdev["lm_head"]
+    tok = list(pr.wl.start)
+    for t in range(pr.wl.steps):
+        pos = [s + t for s in S]
+        # the final normed state does not depend on the LM head: take it from a first pass
+        r0 = orc.step(pr.kc_o, pr.vc_o, tok, pos, pos, precision="f64", taps=True)
+        for i, (ra, rb) in enumerate(pairs):
+            a = np.asarray(r0.taps["final"][i], np.float64)
+            row = as_u16(torch.from_numpy((a / np.linalg.norm(a)).astype(np.float32)).to(torch.bfloat16))
+            for r in (ra, rb):
+                lm_host[r] = row
+                lm_dev[r] = torch.from_numpy(row.view(np.int16).copy()).view(torch.bfloat16).cuda()
+        r = orc.step(pr.kc_o, pr.vc_o, tok, pos, pos, precision="f64")
+        lg, nx = pr.gpu_step(tok, pos, pos)
+        for i, (ra, rb) in enumerate(pairs):
+            assert r.logits[i][ra] == r.logits[i][rb] and r.next_ids[i] == ra, "the oracle does not see the tie"
+            assert lg[i][ra] == lg[i][rb], f"step {t} lane {i}: rows {ra}, {rb} are not an exact tie on the GPU"
+            assert lg[i][ra] == lg[i].max()
+            assert int(nx[i]) == ra, f"step {t} lane {i}: tie broken towards {int(nx[i])}, not row {ra}"
+            check_greedy(lg[i], nx[i], r.logits[i], r.next_ids[i], f"step {t} lane {i}")
+        tok = [int(v) for v in r.next_ids]
+    pr.close()
