@@ -160,6 +160,29 @@ fm_status fm_decode_step_multilaunch(fm_handle *h, const int32_t *token_ids,
                                      const int32_t *positions, const int32_t *kv_lens,
                                      float *logits_out, int32_t *next_ids, hipStream_t stream);
 
+/* Size of the fixed device scratch that fm_decode_step_noalloc uses (each GPU holds one copy
+ * for the life of the process). */
+#define FM_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* For callers that cannot allocate device memory while they run steps (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation). The same step as
+ * fm_decode_step, with the same arguments, results and errors, bit-identical outputs, and the
+ * same kernels; but its per-step scratch (tagged activation words, split-KV partials, argmax
+ * words, LM-head arrival counter) lives in a fixed device array of FM_NOALLOC_SCRATCH_BYTES
+ * instead of the handle's own buffers, and the call makes no allocation of any kind.
+ * Every handle on one GPU shares that GPU's array, which keeps the last step's contents: each
+ * call clears what must start at zero (with a small kernel, so the call can be captured), and
+ * steps tell their own words from stale ones by an epoch counter shared by all handles of the
+ * device. Calls that overlap on one GPU (on different streams, or from different threads
+ * without stream order between them) race on the array and give undefined results.
+ * Returns FM_ERR_CAPACITY, without launching anything, when the handle's step needs more than
+ * FM_NOALLOC_SCRATCH_BYTES (fm_noalloc_scratch_bytes tells how much it needs; batch-1 shapes
+ * up to 13B parameters fit). */
+fm_status fm_decode_step_noalloc(fm_handle *h, const int32_t *token_ids, const int32_t *positions,
+                                 const int32_t *kv_lens, float *logits_out, int32_t *next_ids,
+                                 hipStream_t stream);
+size_t fm_noalloc_scratch_bytes(const fm_handle *h);
+
 /* Prompt extension (prefill) as a loop of single-token steps, the way the paper's serving
  * integration runs an extend batch (Sec. 4.3, deployment in a serving engine): n_tokens
  * decode steps of all b lanes, launched back to back on `stream` with no host

@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -17,6 +18,42 @@
 using namespace fm;
 using namespace fm::dev;
 
+// Fixed device scratch of fm_decode_step_noalloc: the step's tagged activation words, split-KV
+// partials, argmax words and LM-head arrival counter, in place of the handle's own. Every GPU
+// the library runs on holds one copy until the process ends. Host code never passes `scratch`
+// itself to a kernel (in host code the name is a host-side stand-in): it uses the per-device
+// address from hipGetSymbolAddress, kept in g_scratch[].
+static __device__ __align__(256) unsigned char scratch[FM_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};    // device address of `scratch`, per device
+u32 g_scratch_epoch[kMaxDevices] = {};  // step epoch shared by every handle using that copy
+
+// Looks up this device's copy of `scratch` once (the device must be current). Returns null
+// on failure.
+void* scratch_address(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch[dev] = ptr;
+  }
+  return g_scratch[dev];
+}
+
+// Clears the arrival counter and argmax words of the fixed scratch before a step that uses it
+// (a step that ended early leaves them set). A kernel, not a memset, so the call stays
+// capturable.
+__global__ void clear_words(u32* w, int n) {
+  for (int k = threadIdx.x; k < n; k += blockDim.x) w[k] = 0u;
+}
+
+}  // namespace
+
 struct fm_handle {
   fm_model_cfg cfg{};
   int device = 0;
@@ -25,6 +62,8 @@ struct fm_handle {
   int B = 1;
   Params base{};
   Params* d_params = nullptr;
+  Params* d_params_noalloc = nullptr;   // Params with the fixed scratch's buffers; null if it does not fit
+  size_t noalloc_bytes = 0;             // bytes of the fixed scratch this handle's steps use
   float* taps = nullptr;
   u64* timeline = nullptr;
   LayerPtrs* d_layers = nullptr;
@@ -59,6 +98,7 @@ void free_handle(fm_handle* h) {
   hipFree(h->d_layers); hipFree(h->d_rope); hipFree(h->d_instrs); hipFree(h->d_qoff);
   hipFree(h->d_stage); hipFree(h->d_act); hipFree(h->d_part);
   hipFree(h->d_amax); hipFree(h->d_lm_arrive); hipFree(h->d_abort); hipFree(h->d_params); hipFree(h->d_zero);
+  hipFree(h->d_params_noalloc);
   if (h->h_err) hipHostFree(h->h_err);
   delete h;
 }
@@ -90,16 +130,39 @@ hipError_t upload(T** dst, const T* src, size_t n) {
   return n ? hipMemcpy(*dst, src, sizeof(T) * n, hipMemcpyHostToDevice) : hipSuccess;
 }
 
+enum class Mode { Single, PerStage, NoAlloc };
+
 fm_status launch(fm_handle* h, const int32_t* tok, const int32_t* pos, const int32_t* kvl,
-                 float* logits, int32_t* next_ids, hipStream_t stream, bool multi) {
+                 float* logits, int32_t* next_ids, hipStream_t stream, Mode mode) {
   if (!h) return FM_ERR_INVALID_ARG;
   if (!tok || !pos || !kvl || !next_ids) return FM_ERR_INVALID_ARG;
   if (__atomic_load_n(h->h_err, __ATOMIC_ACQUIRE) != 0) return FM_ERR_DEVICE;
-  if (++h->epoch == 0) h->epoch = 1;
+  const bool multi = mode == Mode::PerStage;
+  const Params* dp = h->d_params;
+  u32 epoch = 0;
+  if (mode == Mode::NoAlloc) {
+    if (!h->d_params_noalloc) return FM_ERR_CAPACITY;
+    u32* words = nullptr;
+    {
+      std::lock_guard<std::mutex> lk(g_scratch_mu);
+      words = (u32*)g_scratch[h->device];
+      u32& e = g_scratch_epoch[h->device];
+      if (++e == 0) e = 1;
+      epoch = e;
+    }
+    // the arrival counter and the argmax words start at zero in every step
+    int n_words = 128;
+    void* cargs[] = {&words, &n_words};
+    if (hipLaunchKernel((const void*)clear_words, dim3(1), dim3(64), cargs, 0, stream) != hipSuccess)
+      return FM_ERR_HIP;
+    dp = h->d_params_noalloc;
+  } else {
+    if (++h->epoch == 0) h->epoch = 1;
+    epoch = h->epoch;
+  }
   Step st{};
   st.tok = tok; st.pos = pos; st.kvl = kvl; st.logits = logits; st.next_ids = next_ids;
-  st.taps = h->taps; st.timeline = h->timeline; st.epoch = h->epoch;
-  const Params* dp = h->d_params;
+  st.taps = h->taps; st.timeline = h->timeline; st.epoch = epoch;
   if (!multi) {
     st.stage = -1;
     void* args[] = {&dp, &st};
@@ -291,20 +354,46 @@ fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_k
   p.tap_o = (int32_t)t.o; p.tap_x1 = (int32_t)t.x1; p.tap_a2 = (int32_t)t.a2; p.tap_mlp = (int32_t)t.mlp;
   p.tap_x2 = (int32_t)t.x2;
   HIP_TRY(upload(&h->d_params, &h->base, 1));
+  {
+    // The same parameters over the fixed scratch, for fm_decode_step_noalloc:
+    // [arrival counter: 256 B][argmax words: 256 B][activation words][split-KV partials].
+    const size_t act_off = 512, part_off = act_off + (((size_t)words * 8 + 255) & ~(size_t)255);
+    const size_t need = part_off + part_words * 8;
+    h->noalloc_bytes = need;
+    void* base = scratch_address(dev);
+    if (!base) { free_handle(h); return FM_ERR_HIP; }
+    if (need <= (size_t)FM_NOALLOC_SCRATCH_BYTES) {
+      Params q = h->base;
+      unsigned char* b8 = (unsigned char*)base;
+      q.lm_arrive = (u32*)b8;
+      q.amax = (u64*)(b8 + 256);
+      q.act = (u64*)(b8 + act_off);
+      q.part = (u64*)(b8 + part_off);
+      HIP_TRY(upload(&h->d_params_noalloc, &q, 1));
+    }
+  }
   *out = h;
   return FM_OK;
 }
 
 fm_status fm_decode_step(fm_handle* h, const int32_t* token_ids, const int32_t* positions,
                          const int32_t* kv_lens, float* logits_out, int32_t* next_ids, hipStream_t stream) {
-  return launch(h, token_ids, positions, kv_lens, logits_out, next_ids, stream, false);
+  return launch(h, token_ids, positions, kv_lens, logits_out, next_ids, stream, Mode::Single);
 }
 
 fm_status fm_decode_step_multilaunch(fm_handle* h, const int32_t* token_ids, const int32_t* positions,
                                      const int32_t* kv_lens, float* logits_out, int32_t* next_ids,
                                      hipStream_t stream) {
-  return launch(h, token_ids, positions, kv_lens, logits_out, next_ids, stream, true);
+  return launch(h, token_ids, positions, kv_lens, logits_out, next_ids, stream, Mode::PerStage);
 }
+
+fm_status fm_decode_step_noalloc(fm_handle* h, const int32_t* token_ids, const int32_t* positions,
+                                 const int32_t* kv_lens, float* logits_out, int32_t* next_ids,
+                                 hipStream_t stream) {
+  return launch(h, token_ids, positions, kv_lens, logits_out, next_ids, stream, Mode::NoAlloc);
+}
+
+size_t fm_noalloc_scratch_bytes(const fm_handle* h) { return h ? h->noalloc_bytes : 0; }
 
 fm_status fm_extend(fm_handle* h, const int32_t* token_ids, const int32_t* positions, const int32_t* kv_lens,
                     int32_t n_tokens, float* logits_out, int32_t* next_ids, hipStream_t stream) {
@@ -313,7 +402,7 @@ fm_status fm_extend(fm_handle* h, const int32_t* token_ids, const int32_t* posit
   for (int32_t t = 0; t < n_tokens; ++t) {
     const size_t r = (size_t)t * b;
     const fm_status s = launch(h, token_ids + r, positions + r, kv_lens + r,
-                               t + 1 == n_tokens ? logits_out : nullptr, next_ids, stream, false);
+                               t + 1 == n_tokens ? logits_out : nullptr, next_ids, stream, Mode::Single);
     if (s != FM_OK) return s;
   }
   return FM_OK;

@@ -46,9 +46,9 @@ class fm_plan_stats(ctypes.Structure):
         ("imbalance", ctypes.c_double)]
 
 
-EXPORTS = ("fm_create", "fm_decode_step", "fm_decode_step_multilaunch", "fm_extend", "fm_destroy", "fm_last_error",
-           "fm_set_taps", "fm_tap_count", "fm_set_timeline", "fm_instruction_count", "fm_plan_query",
-           "fm_plan_export", "fm_status_string")
+EXPORTS = ("fm_create", "fm_decode_step", "fm_decode_step_multilaunch", "fm_decode_step_noalloc", "fm_extend",
+           "fm_destroy", "fm_last_error", "fm_set_taps", "fm_tap_count", "fm_set_timeline", "fm_instruction_count",
+           "fm_noalloc_scratch_bytes", "fm_plan_query", "fm_plan_export", "fm_status_string")
 
 _lib = None
 
@@ -64,8 +64,10 @@ def load():
     P, I32 = ctypes.c_void_p, ctypes.c_int32
     L.fm_create.argtypes = [ctypes.POINTER(fm_model_cfg), ctypes.POINTER(fm_weight_ptrs),
                             ctypes.POINTER(fm_kv_ptrs), ctypes.POINTER(P)]
-    for n in ("fm_decode_step", "fm_decode_step_multilaunch"):
+    for n in ("fm_decode_step", "fm_decode_step_multilaunch", "fm_decode_step_noalloc"):
         getattr(L, n).argtypes = [P, P, P, P, P, P, P]
+    L.fm_noalloc_scratch_bytes.argtypes = [P]
+    L.fm_noalloc_scratch_bytes.restype = ctypes.c_size_t
     L.fm_extend.argtypes = [P, P, P, P, I32, P, P, P]
     L.fm_destroy.argtypes = [P]
     L.fm_last_error.argtypes = [P, ctypes.POINTER(I32)]
@@ -79,7 +81,7 @@ def load():
     L.fm_status_string.argtypes = [I32]
     L.fm_status_string.restype = ctypes.c_char_p
     for n in EXPORTS:
-        if n not in ("fm_tap_count", "fm_status_string"):
+        if n not in ("fm_tap_count", "fm_status_string", "fm_noalloc_scratch_bytes"):
             getattr(L, n).restype = I32
     _lib = L
     return L
@@ -170,12 +172,16 @@ class Decoder:
         self.h = h
         self._taps = None
 
-    def step(self, token_ids, positions, kv_lens, logits_out, next_ids, stream=None, multilaunch=False):
-        """All arguments are CUDA tensors (int32 / float32); stream defaults to torch's current stream."""
+    def step(self, token_ids, positions, kv_lens, logits_out, next_ids, stream=None, multilaunch=False,
+             noalloc=False):
+        """All arguments are CUDA tensors (int32 / float32); stream defaults to torch's current stream.
+        ``multilaunch``: the per-stage ablation; ``noalloc``: fm_decode_step_noalloc."""
         import torch
         if stream is None:
             stream = torch.cuda.current_stream().cuda_stream
-        fn = load().fm_decode_step_multilaunch if multilaunch else load().fm_decode_step
+        assert not (multilaunch and noalloc)
+        fn = (load().fm_decode_step_multilaunch if multilaunch else
+              load().fm_decode_step_noalloc if noalloc else load().fm_decode_step)
         st = fn(self.h, token_ids.data_ptr(), positions.data_ptr(), kv_lens.data_ptr(),
                 logits_out.data_ptr() if logits_out is not None else None, next_ids.data_ptr(), stream)
         check(st, "fm_decode_step")
@@ -195,6 +201,9 @@ class Decoder:
                               int(token_ids.shape[0]), logits_out.data_ptr() if logits_out is not None else None,
                               next_ids.data_ptr(), stream)
         check(st, "fm_extend")
+
+    def noalloc_scratch_bytes(self) -> int:
+        return int(load().fm_noalloc_scratch_bytes(self.h))
 
     def set_taps(self, tap_buf):
         self._taps = tap_buf

@@ -66,6 +66,8 @@ def test_null_arguments_rejected(fm):
     assert L.fm_destroy(None) == INVALID
     assert L.fm_decode_step(None, None, None, None, None, None, None) == INVALID
     assert L.fm_decode_step_multilaunch(None, None, None, None, None, None, None) == INVALID
+    assert L.fm_decode_step_noalloc(None, None, None, None, None, None, None) == INVALID
+    assert L.fm_noalloc_scratch_bytes(None) == 0
     assert L.fm_extend(None, None, None, None, 1, None, None, None) == INVALID
     code = ctypes.c_int32(0)
     assert L.fm_last_error(None, ctypes.byref(code)) == INVALID
