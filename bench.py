@@ -81,7 +81,7 @@ def measure(name: str, args, context: int = 0, cpu: bool = False, ablation: bool
     wdev = {k: v for k, v in wl.weights.items() if k != "layers" and v is not None}
     wdev["layers"] = list(wl.weights["layers"])
     kc, vc = list(wl.kcache), list(wl.vcache)
-    dec = Decoder(cfg, wdev, kc, vc, n_workgroups=args.nwg, attn_items=args.attn_items)
+    dec = Decoder(cfg, wdev, kc, vc, n_workgroups=args.nwg, attn_items=args.attn_items, dyn_chunk_kb=args.dyn_chunk_kb)
 
     S = wl.S
     pos_all = torch.tensor([[s + t for s in S] for t in range(total_steps)], dtype=torch.int32, device="cuda")
@@ -219,6 +219,8 @@ def main():
                     help="also run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--nwg", type=int, default=0)
     ap.add_argument("--attn-items", type=int, default=0)
+    ap.add_argument("--dyn-chunk-kb", type=int, default=0,
+                    help="weight KiB per dynamically claimed GEMV chunk (0 automatic, -1 fixed tiles only)")
     ap.add_argument("--context", type=int, default=0,
                     help="prefilled context of every lane, overriding the workload's (a context sweep)")
     args = ap.parse_args()

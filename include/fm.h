@@ -64,7 +64,9 @@ enum {
   FM_DEV_BAD_TOKEN = 1,     /* token_ids[i] outside [0, vocab) */
   FM_DEV_BAD_POSITION = 2,  /* positions[i] outside [0, max_ctx) */
   FM_DEV_BAD_KV_LEN = 3,    /* kv_lens[i] outside [0, max_ctx - 1] */
-  FM_DEV_WATCHDOG = 4       /* a dependency wait exceeded its time bound */
+  FM_DEV_WATCHDOG = 4,      /* a dependency wait exceeded its time bound */
+  FM_DEV_BAD_PLAN = 5       /* an instruction's geometry does not fit the kernel's LDS layout
+                               (cannot happen with a schedule built by fm_create) */
 };
 
 /* Model shape, batch and context bound (the model configuration the schedule is compiled
@@ -82,7 +84,9 @@ typedef struct fm_model_cfg {
   /* Tuning (0 = automatic; the automatic values are the measured best on MI355X): */
   int32_t n_workgroups;     /* persistent workgroups; 0 = one per compute unit */
   int32_t attn_items;       /* attention work items per layer; 0 = about one per workgroup */
-  int32_t reserved;         /* must be 0 */
+  int32_t dyn_chunk_kb;     /* weight KiB per chunk of a QKV, O-projection or down stage split
+                               into chunks that the workgroups claim at run time; 0 = automatic
+                               (128), -1 = every GEMV stage in fixed per-workgroup tiles */
   double rope_theta;        /* RoPE base */
   double rms_eps;           /* RMSNorm epsilon, inside the square root */
 } fm_model_cfg;
@@ -239,7 +243,9 @@ size_t fm_tap_count(const fm_model_cfg *cfg);
  * wall-clock ticks {start, inputs ready, prologue done, stream done, end, workgroup, a, b}.
  * For attention items the middle marks are: q/k/v ready, rotary and KV append done, partials
  * published; the span from there to the end is the group merge (last item of a group only);
- * a = the item's slot passes done, b = its waves' partials gathered in LDS (0 for GEMV tiles).
+ * a = the item's slot passes done, b = its waves' partials gathered in LDS. GEMV tiles leave
+ * a and b 0, except that a GEMV stage in dynamic chunks records in a the number of chunks the
+ * workgroup took (a count, not a time).
  * Marks an instruction does not reach are 0. The ticks are from the 100 MHz constant clock,
  * read with s_memrealtime. These spans give the paper's busy fraction and tail spread
  * (Sec. 4.1, dependency gate). Pass NULL to turn the timeline off. */
@@ -250,7 +256,17 @@ int32_t fm_instruction_count(const fm_handle *h);
  * streams that the host compiles from the model (Sec. 4.1, first step).
  *   fm_plan_query fills the summary statistics. n_cu is the workgroup count to plan for.
  *   fm_plan_export copies the queues: qoff (int32[n_cu + 1]) gives queue w's range in
- *   instrs, and instrs holds int32[4] records {op, layer, a, b} (FM_OP_*).
+ *   instrs, and instrs holds int32[4] records {op, layer, a, b} (FM_OP_*):
+ *     GEMV, a >= 0: output rows [a, b) of the op's matrix, streamed by this workgroup alone;
+ *     GEMV, a < 0 (QKV, O projection, down; batch <= 2): a stage in dynamic chunks of -a
+ *       rows. Every workgroup holds one such
+ *       record per stage. Workgroup w serves pool w mod P (P = min(8, n_cu)); the stage's
+ *       ceil(rows / -a) chunks are split into contiguous pool ranges in proportion to the
+ *       pools' workgroup counts. Each workgroup of a pool takes one chunk of the range (its
+ *       (w div P)-th), and the range's other chunks go to the pool's workgroups on demand,
+ *       through one device counter per (stage, pool). b packs the chunk's K split (b & 255)
+ *       and the most chunks one workgroup may take (b >> 8).
+ *     FM_OP_ATTN: attention work item a of the layer.
  *   Its return codes: FM_ERR_CAPACITY when the arrays are shorter than fm_plan_query
  *   reports; FM_ERR_INVALID_ARG or FM_ERR_UNSUPPORTED for a bad cfg. */
 enum { FM_OP_QKV = 1, FM_OP_ATTN = 2, FM_OP_OPROJ = 3, FM_OP_GU = 4, FM_OP_DOWN = 5, FM_OP_LM = 6 };
@@ -264,7 +280,9 @@ typedef struct fm_plan_stats {
   int32_t attn_items;        /* attention work items per layer */
   int32_t attn_max_chunks;   /* capacity of split-KV partials per (lane, KV head) */
   int32_t n_stages;          /* launches the multi-launch ablation makes per step */
-  double max_bytes_per_cu;   /* weight bytes streamed by the busiest queue */
+  int32_t n_dyn_stages;      /* GEMV stages run in dynamic chunks */
+  double max_bytes_per_cu;   /* weight bytes streamed by the busiest queue (a dynamic stage
+                                counts its mean share for every queue) */
   double mean_bytes_per_cu;
   double imbalance;          /* max / mean */
 } fm_plan_stats;

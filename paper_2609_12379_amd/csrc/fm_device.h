@@ -55,6 +55,8 @@ template <int B> constexpr int xslab_floats() {
   return LDS_FLOATS - MISC_FLOATS - RESID_FLOATS - rowacc_floats<B>();
 }
 static_assert(kMergeFloats + ATT_FLOATS + MISC_FLOATS <= LDS_FLOATS, "attention LDS layout");
+static_assert(xslab_floats<1>() == kXslabFloatsVALU && xslab_floats<2>() == kXslabFloatsVALU &&
+              rowacc_floats<1>() == kRowaccFloatsVALU, "the scheduler's view of the VALU tile's LDS");
 
 constexpr u32 CPOL_NT = 2;    // non-temporal (streaming)
 constexpr u32 CPOL_SC1 = 16;  // device-scope coherent
@@ -87,6 +89,8 @@ struct Params {
   u64* part;                     // tagged [L][b][nh][maxc][d + 2]: split-KV partials
   u64* amax;                     // [b]
   u32* lm_arrive;                // [1]
+  u32* dyn_ctr;                  // [kPools][dyn_stride]: claim counters of dynamic GEMV stages
+  int32_t dyn_stride;            // counters per pool (one per GEMV stage, padded to 128 bytes)
   u32* abort_flag;               // [1]
   u32* err_host;                 // pinned host word
   int64_t tap_block;             // floats per (layer, lane) block

@@ -54,6 +54,14 @@ __global__ __launch_bounds__(NT, 1) void step_kernel(const Params* __restrict__ 
     bool ok = true;
     if (op == FM_OP_ATTN) {
       ok = op_attn<D, GT>(P, st, ins, smem, tid, lane, wave, tl);
+    } else if (ins[2] < 0) {
+      // A QKV, O-projection or down stage in dynamic chunks (VALU tiles only).
+      if constexpr (B <= 2) {
+        ok = op_gemv_dyn<B>(P, st, ins, smem, tid, lane, wave, tl);
+      } else {
+        if (tid == 0) raise_error(P, FM_DEV_BAD_PLAN);
+        ok = false;
+      }
     } else if (op == FM_OP_GU) {
       ok = op_gemv<B, 2>(P, st, ins, smem, tid, lane, wave, tl);
     } else {

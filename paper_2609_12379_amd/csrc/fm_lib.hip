@@ -19,7 +19,8 @@ using namespace fm;
 using namespace fm::dev;
 
 // Fixed device scratch of fm_decode_step_noalloc: the step's tagged activation words, split-KV
-// partials, argmax words and LM-head arrival counter, in place of the handle's own. Every GPU
+// partials, argmax words, LM-head arrival counter and chunk claim counters, in place of the
+// handle's own. Every GPU
 // the library runs on holds one copy until the process ends. Host code never passes `scratch`
 // itself to a kernel (in host code the name is a host-side stand-in): it uses the per-device
 // address from hipGetSymbolAddress, kept in g_scratch[].
@@ -45,9 +46,9 @@ void* scratch_address(int dev) {
   return g_scratch[dev];
 }
 
-// Clears the arrival counter and argmax words of the fixed scratch before a step that uses it
-// (a step that ended early leaves them set). A kernel, not a memset, so the call stays
-// capturable.
+// Clears the arrival counter, argmax words and claim counters of the fixed scratch before a
+// step that uses it (another handle's step may have left other data there). A kernel, not a
+// memset, so the call stays capturable.
 __global__ void clear_words(u32* w, int n) {
   for (int k = threadIdx.x; k < n; k += blockDim.x) w[k] = 0u;
 }
@@ -64,6 +65,7 @@ struct fm_handle {
   Params* d_params = nullptr;
   Params* d_params_noalloc = nullptr;   // Params with the fixed scratch's buffers; null if it does not fit
   size_t noalloc_bytes = 0;             // bytes of the fixed scratch this handle's steps use
+  int noalloc_clear_words = 0;          // leading words of it cleared before each step
   float* taps = nullptr;
   u64* timeline = nullptr;
   LayerPtrs* d_layers = nullptr;
@@ -73,6 +75,7 @@ struct fm_handle {
   u64* d_part = nullptr;
   u64* d_amax = nullptr;
   u32* d_lm_arrive = nullptr;
+  u32* d_dyn = nullptr;    // claim counters of the dynamic GEMV stages
   u32* d_abort = nullptr;
   uint16_t* d_zero = nullptr;
   u32* h_err = nullptr;   // pinned, device-visible
@@ -97,7 +100,7 @@ void free_handle(fm_handle* h) {
   if (!h) return;
   hipFree(h->d_layers); hipFree(h->d_rope); hipFree(h->d_instrs); hipFree(h->d_qoff);
   hipFree(h->d_stage); hipFree(h->d_act); hipFree(h->d_part);
-  hipFree(h->d_amax); hipFree(h->d_lm_arrive); hipFree(h->d_abort); hipFree(h->d_params); hipFree(h->d_zero);
+  hipFree(h->d_amax); hipFree(h->d_lm_arrive); hipFree(h->d_dyn); hipFree(h->d_abort); hipFree(h->d_params); hipFree(h->d_zero);
   hipFree(h->d_params_noalloc);
   if (h->h_err) hipHostFree(h->h_err);
   delete h;
@@ -150,10 +153,10 @@ fm_status launch(fm_handle* h, const int32_t* tok, const int32_t* pos, const int
       if (++e == 0) e = 1;
       epoch = e;
     }
-    // the arrival counter and the argmax words start at zero in every step
-    int n_words = 128;
+    // the arrival counter, the argmax words and the claim counters start at zero in every step
+    int n_words = h->noalloc_clear_words;
     void* cargs[] = {&words, &n_words};
-    if (hipLaunchKernel((const void*)clear_words, dim3(1), dim3(64), cargs, 0, stream) != hipSuccess)
+    if (hipLaunchKernel((const void*)clear_words, dim3(1), dim3(256), cargs, 0, stream) != hipSuccess)
       return FM_ERR_HIP;
     dp = h->d_params_noalloc;
   } else {
@@ -316,6 +319,11 @@ fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_k
   HIP_TRY(hipMemset(h->d_amax, 0, b * 8));
   HIP_TRY(hipMalloc(&h->d_lm_arrive, 64));
   HIP_TRY(hipMemset(h->d_lm_arrive, 0, 64));
+  // One counter per (GEMV stage, pool); each pool's counters on their own 128-byte lines.
+  const int32_t dyn_stride = ((4 * (int32_t)L + 1) + 31) / 32 * 32;
+  const size_t dyn_bytes = (size_t)kPools * dyn_stride * 4;
+  HIP_TRY(hipMalloc(&h->d_dyn, dyn_bytes));
+  HIP_TRY(hipMemset(h->d_dyn, 0, dyn_bytes));
   HIP_TRY(hipMalloc(&h->d_zero, 65536));
   HIP_TRY(hipMemset(h->d_zero, 0, 65536));
   HIP_TRY(hipMalloc(&h->d_abort, 64));
@@ -347,6 +355,7 @@ fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_k
   p.off_m = p.off_x1 + (u32)L * p.st_x1;
   p.zero_page = h->d_zero;
   p.part = h->d_part; p.amax = h->d_amax; p.lm_arrive = h->d_lm_arrive;
+  p.dyn_ctr = h->d_dyn; p.dyn_stride = dyn_stride;
   p.abort_flag = h->d_abort; p.err_host = h->d_err;
   const TapOff t = tap_offsets(c);
   p.tap_block = t.block;
@@ -356,8 +365,11 @@ fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_k
   HIP_TRY(upload(&h->d_params, &h->base, 1));
   {
     // The same parameters over the fixed scratch, for fm_decode_step_noalloc:
-    // [arrival counter: 256 B][argmax words: 256 B][activation words][split-KV partials].
-    const size_t act_off = 512, part_off = act_off + (((size_t)words * 8 + 255) & ~(size_t)255);
+    // [arrival counter: 256 B][argmax words: 256 B][claim counters][activation words][split-KV
+    // partials]. Everything before the activation words is cleared before each such step.
+    const size_t dyn_off = 512, act_off = dyn_off + ((dyn_bytes + 255) & ~(size_t)255);
+    const size_t part_off = act_off + (((size_t)words * 8 + 255) & ~(size_t)255);
+    h->noalloc_clear_words = (int)(act_off / 4);
     const size_t need = part_off + part_words * 8;
     h->noalloc_bytes = need;
     void* base = scratch_address(dev);
@@ -367,6 +379,7 @@ fm_status fm_create(const fm_model_cfg* cfg, const fm_weight_ptrs* w, const fm_k
       unsigned char* b8 = (unsigned char*)base;
       q.lm_arrive = (u32*)b8;
       q.amax = (u64*)(b8 + 256);
+      q.dyn_ctr = (u32*)(b8 + dyn_off);
       q.act = (u64*)(b8 + act_off);
       q.part = (u64*)(b8 + part_off);
       HIP_TRY(upload(&h->d_params_noalloc, &q, 1));

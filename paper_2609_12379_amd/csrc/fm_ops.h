@@ -299,48 +299,118 @@ __device__ __forceinline__ const uint16_t* zero_slot(CParams& p, int wave, int l
   return p.zero_page + ((((int)blockIdx.x * NWAVE + wave) * 64 + lane) & 4095) * 8;
 }
 
+// What a GEMV operator reads and writes: its matrices, input vector, norm and residual.
+struct GemvOperand {
+  int K = 0, rows = 0;              // columns and output rows of the operator's matrix
+  int sidx = 0;                     // claim counter of its stage (dynamic chunks)
+  const uint16_t* gain = nullptr;   // RMSNorm gain (norm prologue) or null
+  bool from_embed = false;          // input is the embedding row (layer 0 QKV)
+  u32 in_w = 0, in_stride = 0;      // tagged input: word offset of lane 0, words per lane
+  u32 res_w = 0, res_stride = 0;    // tagged residual (OPROJ, DOWN)
+  bool res_embed = false, has_res = false;
+  const uint16_t* m0 = nullptr;     // matrices: QKV uses m0..m2 (W_q, W_k, W_v), GU m0, m1
+  const uint16_t* m1 = nullptr;
+  const uint16_t* m2 = nullptr;
+};
+
+__device__ __forceinline__ GemvOperand gemv_operand(CParams& p, int op, int l) {
+  const int nq = p.nh * p.d, nk = p.nkv * p.d;
+  CLayerPtrs* Lw = (op == FM_OP_LM) ? nullptr : (CLayerPtrs*)p.layers + l;
+  GemvOperand o;
+  switch (op) {
+    case FM_OP_QKV:
+      o.K = p.h; o.rows = nq + 2 * nk; o.sidx = 4 * l; o.gain = Lw->attn_norm;
+      if (l == 0) o.from_embed = true; else { o.in_w = p.off_x + (u32)l * p.st_x; o.in_stride = p.h; }
+      o.m0 = Lw->wq; o.m1 = Lw->wk; o.m2 = Lw->wv;
+      break;
+    case FM_OP_OPROJ:
+      o.K = nq; o.rows = p.h; o.sidx = 4 * l + 1; o.in_w = p.off_o + (u32)l * p.st_o; o.in_stride = nq;
+      o.has_res = true;
+      if (l == 0) o.res_embed = true; else { o.res_w = p.off_x + (u32)l * p.st_x; o.res_stride = p.h; }
+      o.m0 = Lw->wo;
+      break;
+    case FM_OP_GU:
+      o.K = p.h; o.rows = p.inter; o.sidx = 4 * l + 2; o.gain = Lw->mlp_norm;
+      o.in_w = p.off_x1 + (u32)l * p.st_x1; o.in_stride = p.h;
+      o.m0 = Lw->wg; o.m1 = Lw->wu;
+      break;
+    case FM_OP_DOWN:
+      o.K = p.inter; o.rows = p.h; o.sidx = 4 * l + 3; o.in_w = p.off_m + (u32)l * p.st_m; o.in_stride = p.inter;
+      o.has_res = true; o.res_w = p.off_x1 + (u32)l * p.st_x1; o.res_stride = p.h;
+      o.m0 = Lw->wd;
+      break;
+    default:  // FM_OP_LM
+      o.K = p.h; o.rows = p.V; o.sidx = 4 * p.L; o.gain = p.final_norm;
+      o.in_w = p.off_x + (u32)p.L * p.st_x; o.in_stride = p.h;
+      o.m0 = p.lm_head;
+      break;
+  }
+  return o;
+}
+
+// Clears the claim counters of the dynamic GEMV stages for the next step. Called by the
+// workgroup that completes the step's LM head: every workgroup has made its last claim by
+// then, since each stores its rows only after its last claim of the stage has returned.
+__device__ __forceinline__ void reset_claims(CParams& p, int tid) {
+  for (int k = tid; k < kPools * p.dyn_stride; k += NT)
+    __hip_atomic_store(p.dyn_ctr + k, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// End of an LM-head instruction: the workgroup folds its lanes' packed keys (key[i], one per
+// thread) into one per batch lane with an integer max, applies it to the step's maximum with
+// an atomic max, and counts itself in. The workgroup that arrives last (all maxima performed)
+// writes the greedy tokens and resets the step's counters.
+template <int B>
+__device__ __forceinline__ void lm_finish(CParams& p, const Step& st, const u64 (&key)[B], float* misc, int tid,
+                                          int lane, int wave) {
+  u64* wkeys = reinterpret_cast<u64*>(misc + 16);   // [NWAVE][B]
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    const u64 k = wave_max_u64(key[i]);
+    if (lane == 0) wkeys[wave * B + i] = k;
+  }
+  __syncthreads();
+  // One thread per batch lane folds the waves' keys into the step's maximum (all lanes'
+  // atomics in flight together), and waits until its atomic has been performed.
+  if (tid < p.b) {
+    u64 k = 0;
+    for (int w = 0; w < NWAVE; ++w) k = wkeys[w * B + tid] > k ? wkeys[w * B + tid] : k;
+    if (k) __hip_atomic_fetch_max(p.amax + tid, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    vm_wait0();
+  }
+  __syncthreads();
+  int* last = reinterpret_cast<int*>(misc + 8);
+  if (tid == 0) {
+    const u32 old = __hip_atomic_fetch_add(p.lm_arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int is_last = old == (u32)p.n_lm_instr - 1u ? 1 : 0;
+    if (is_last) __hip_atomic_store(p.lm_arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *last = is_last;
+  }
+  __syncthreads();
+  if (*last) {
+    if (tid < p.b) {
+      const u64 k = __hip_atomic_load(p.amax + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      st.next_ids[tid] = (int32_t)(0xFFFFFFFFu - (u32)(k & 0xFFFFFFFFull));
+      __hip_atomic_store(p.amax + tid, (u64)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    reset_claims(p, tid);
+  }
+}
+
 template <int B, int NW>
 __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_t* ins, float* smem, int tid,
                                         int lane, int wave, u64* tl) {
   const int op = uni(ins[0]), l = uni(ins[1]), ra = uni(ins[2]), rb = uni(ins[3]);
   const int nr = rb - ra;
   const int nq = p.nh * p.d, nk = p.nkv * p.d, nqkv = nq + 2 * nk;
-  CLayerPtrs* Lw = (op == FM_OP_LM) ? nullptr : (CLayerPtrs*)p.layers + l;
 
   // Operator geometry.
-  int K = 0;
-  const uint16_t* gain = nullptr;   // RMSNorm gain (norm prologue) or null
-  bool from_embed = false;          // input is the embedding row (layer 0 QKV)
-  u32 in_w = 0, in_stride = 0;      // tagged input: word offset of lane 0, words per lane
-  u32 res_w = 0, res_stride = 0;    // tagged residual (OPROJ, DOWN)
-  bool res_embed = false, has_res = false;
-  const uint16_t* m0 = nullptr; const uint16_t* m1 = nullptr; const uint16_t* m2 = nullptr;
-  switch (op) {
-    case FM_OP_QKV:
-      K = p.h; gain = Lw->attn_norm;
-      if (l == 0) from_embed = true; else { in_w = p.off_x + (u32)l * p.st_x; in_stride = p.h; }
-      m0 = Lw->wq; m1 = Lw->wk; m2 = Lw->wv;
-      break;
-    case FM_OP_OPROJ:
-      K = nq; in_w = p.off_o + (u32)l * p.st_o; in_stride = nq;
-      has_res = true;
-      if (l == 0) res_embed = true; else { res_w = p.off_x + (u32)l * p.st_x; res_stride = p.h; }
-      m0 = Lw->wo;
-      break;
-    case FM_OP_GU:
-      K = p.h; gain = Lw->mlp_norm; in_w = p.off_x1 + (u32)l * p.st_x1; in_stride = p.h;
-      m0 = Lw->wg; m1 = Lw->wu;
-      break;
-    case FM_OP_DOWN:
-      K = p.inter; in_w = p.off_m + (u32)l * p.st_m; in_stride = p.inter;
-      has_res = true; res_w = p.off_x1 + (u32)l * p.st_x1; res_stride = p.h;
-      m0 = Lw->wd;
-      break;
-    default:  // FM_OP_LM
-      K = p.h; gain = p.final_norm; in_w = p.off_x + (u32)p.L * p.st_x; in_stride = p.h;
-      m0 = p.lm_head;
-      break;
-  }
+  const GemvOperand opd = gemv_operand(p, op, l);
+  const int K = opd.K;
+  const uint16_t* gain = opd.gain;
+  const bool from_embed = opd.from_embed, res_embed = opd.res_embed, has_res = opd.has_res;
+  const u32 in_w = opd.in_w, in_stride = opd.in_stride, res_w = opd.res_w, res_stride = opd.res_stride;
+  const uint16_t* m0 = opd.m0; const uint16_t* m1 = opd.m1; const uint16_t* m2 = opd.m2;
   const __amdgpu_buffer_rsrc_t ract = rsrc(p.act, p.act_bytes);
 
   // Geometry (all wave-uniform).
@@ -693,39 +763,337 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
 
   // 5. LM head: one packed key per lane per tile via an integer max (order-independent),
   //    then the last LM tile of the step writes the greedy tokens.
-  if (op == FM_OP_LM) {
-    u64* wkeys = reinterpret_cast<u64*>(misc + 16);   // [NWAVE][B]
+  if (op == FM_OP_LM) lm_finish<B>(p, st, key, misc, tid, lane, wave);
+  __syncthreads();   // LDS is reused by the next instruction
+  return true;
+}
+
+// ---- GEMV stage in dynamic chunks (VALU tiles, B <= 2) -----------------------------------
+//
+// With one fixed tile per workgroup a stage ends when its slowest tile does, and which tiles
+// stream slowly changes from stage to stage. Large VALU stages of the QKV, O-projection and
+// down operators are therefore cut into chunks of Rc output rows, grouped into pools: workgroup w serves pool w mod 8 (on MI355X, the
+// workgroups that share one XCD's L2). Each workgroup takes one chunk of its pool's range as
+// its own; the range's other chunks go to the pool's workgroups as they ask for them, through
+// one atomic counter per (stage, pool), so a workgroup that runs late takes fewer chunks.
+// Every chunk is computed the same way whoever takes it (same K split, same order of sums),
+// so the results do not depend on the assignment.
+//
+// A chunk is Rc = 4 * 8 / KP rows split into KP parts along K: exactly one (row quad,
+// K part) item per wave, the same one in every chunk, SP segments of 128 columns long. A wave
+// thus streams SP units per chunk through one register ring, with no barrier between chunks:
+// the chunk ids sit in an LDS list that wave 0 fills. Wave 0 claims the next chunk during the
+// last ring rounds of the current one (at a round start, publishing the answer at the next
+// round start, when the claim is older than the ring's U loads in flight and the publication
+// does not wait). Row part sums stay in LDS per chunk; the epilogue writes all of the
+// workgroup's rows once its last chunk is done, after its last claim has returned.
+
+typedef __attribute__((address_space(3))) volatile int lds_int;
+
+template <int B>
+__device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const int32_t* ins, float* smem, int tid,
+                                            int lane, int wave, u64* tl) {
+  static_assert(B <= 2 && NCTL == 0, "dynamic chunks run VALU tiles streamed by every wave");
+  constexpr int U = FM_RING;
+  constexpr int UNKNOWN = -2, END = -1;
+  const int op = uni(ins[0]), l = uni(ins[1]);
+  const int Rc = uni(-ins[2]), KP = uni(ins[3] & 0xff), nslot = uni(ins[3] >> 8);
+  const int nq = p.nh * p.d, nk = p.nkv * p.d, nqkv = nq + 2 * nk;
+  const GemvOperand o = gemv_operand(p, op, l);
+  const int K = o.K, R = o.rows;
+  const int Kpad = uni((K + 127) & ~127), nseg = uni(Kpad / 128);
+  const int NQ = uni(NWAVE / KP), nwr = uni(4 * NQ);
+  const int SP = uni((nseg + KP - 1) / KP);
+  // This wave's item in every chunk: row quad qd, K part pt; sp_ok of its SP segments lie
+  // inside the matrix.
+  const int qd = uni(wave / KP), pt = uni(wave - (wave / KP) * KP);
+  const int sp_ok = uni(max(0, min(SP, nseg - pt * SP)));
+
+  float* xs = smem;                                  // [B][Kpad] input times its gain
+  float* rowacc = smem + xslab_floats<B>();          // [nslot][KP][nwr][B] row part sums
+  float* misc = smem + LDS_FLOATS - MISC_FLOATS;
+  float* mss = misc + 512;                           // [NWAVE][B] partial sums of squares
+  lds_int* chl = (lds_int*)(__attribute__((address_space(3))) int*)(misc + 256);   // [nslot + 1] chunk ids
+
+  // The schedule guarantees these; a violation would overrun LDS, so it stops the step.
+  if (!(op == FM_OP_QKV || op == FM_OP_OPROJ || op == FM_OP_DOWN) || nslot < 2 || nslot > 254 ||
+      !(KP == 1 || KP == 2 || KP == 4 || KP == 8) || Rc != nwr || SP < U ||
+      B * Kpad > xslab_floats<B>() || nslot * KP * nwr * B > rowacc_floats<B>()) {
+    if (tid == 0) raise_error(p, FM_DEV_BAD_PLAN);
+    return false;
+  }
+
+  // This workgroup's pool, its own chunk and the pool's shared range.
+  const int nwg = p.nwg, np = min(kPools, nwg), wg = (int)blockIdx.x;
+  const int px = wg % np, kx = wg / np;
+  const int nwx = (nwg - px + np - 1) / np;
+  const int sx = px * (nwg / np) + min(px, nwg % np);
+  const int nch = (R + Rc - 1) / Rc;
+  const int c0 = (int)((long long)nch * sx / nwg), c1 = (int)((long long)nch * (sx + nwx) / nwg);
+  const int own = uni(c0 + kx), dyn0 = uni(c0 + nwx), ndyn = uni(c1 - c0 - nwx);
+  u32* ctr = p.dyn_ctr + px * p.dyn_stride + o.sidx;
+  if (tid == 0) {
+    chl[0] = own;
+    for (int j = 1; j <= nslot; ++j) chl[j] = (j == nslot || ndyn == 0) ? END : UNKNOWN;
+  }
+
+  // Per lane: weight row wr of the chunk (16 lanes per row), first column kl of its part, and
+  // how many of the part's segments hold columns of this lane inside K.
+  const int wr = qd * 4 + (lane >> 4);
+  const int kl = pt * SP * 128 + (lane & 15) * 8;
+  const int seg_ok = max(0, min(sp_ok, (K - kl + 127) / 128));
+  const uint16_t* zp = zero_slot(p, wave, lane);
+  // Row pointer of chunk c for this lane (at column kl), and its count of loadable segments.
+  auto chunk_row = [&](int c, const uint16_t*& rp, int& lim) {
+    const int r = c * Rc + wr;
+    const uint16_t* m;
+    int rr = r;
+    if (op == FM_OP_QKV) {
+      m = r >= nq + nk ? o.m2 : (r >= nq ? o.m1 : o.m0);
+      rr = r >= nq + nk ? r - nq - nk : (r >= nq ? r - nq : r);
+    } else {
+      m = o.m0;
+    }
+    const bool live = r < R;
+    rp = live ? m + (size_t)rr * K + kl : zp;
+    lim = live ? seg_ok : 0;
+  };
+
+  // Claims (wave 0; lane 0 holds the counter's answer). The next slot is claimed at a round
+  // start once the issue cursor is within 2U units of its chunk's end.
+  const int claim_from = uni(max(0, SP - 2 * U));
+  int pend_slot = -1, claimed = 0;
+  bool exhausted = ndyn == 0;
+  u32 pend = 0;
+  auto publish = [&]() {
+    const u32 v = (u32)uni((int)pend);
+    const int ch = v < (u32)ndyn ? dyn0 + (int)v : END;
+    if (lane == 0) chl[pend_slot] = ch;
+    if (ch < 0) exhausted = true;
+    pend_slot = -1;
+  };
+
+  // Issue cursor: slot i_j, segment i_sg; the lane's row pointer and loadable segments.
+  int i_j = 0, i_sg = 0;
+  bool i_live = true;
+  const uint16_t* i_rp;
+  int i_lim;
+  chunk_row(own, i_rp, i_lim);
+  auto issue = [&](u32x4& dst) {
+    dst = ld_stream16(i_sg < i_lim ? i_rp + i_sg * 128 : zp);
+    i_sg = uni(i_sg + 1);
+    if (i_sg == SP && i_live) {
+      // Next slot: wait (on LDS) until its chunk id is known.
+      i_sg = 0;
+      i_j = uni(i_j + 1);
+      if (wave == 0 && pend_slot == i_j) publish();   // wave 0 caught up with its own claim
+      int v = uni(chl[i_j]);
+      if (v == UNKNOWN) {
+        const u64 t0 = clock_now();
+        while (true) {
+          __builtin_amdgcn_s_sleep(1);
+          v = uni(chl[i_j]);
+          if (v != UNKNOWN) break;
+          if (clock_now() - t0 > WAIT_TICKS) {
+            raise_error(p, FM_DEV_WATCHDOG);
+            v = END;
+            break;
+          }
+        }
+      }
+      if (v < 0) {
+        i_live = false;
+        i_lim = 0;
+      } else {
+        chunk_row(v, i_rp, i_lim);
+      }
+    }
+  };
+
+  // 1. Prefetch U units of the own chunk (SP >= U) and claim the second chunk (the ring's
+  //    first round start comes too late in the own chunk), before waiting for the input.
+  u32x4 ring[U];
 #pragma unroll
-    for (int i = 0; i < B; ++i) {
-      const u64 k = wave_max_u64(key[i]);
-      if (lane == 0) wkeys[wave * B + i] = k;
+  for (int sl = 0; sl < U; ++sl) issue(ring[sl]);
+  if (wave == 0 && !exhausted) {
+    if (lane == 0) pend = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    pend_slot = 1;
+    claimed = 1;
+  }
+
+  // 2. Stage the input times its gain (sum of squares on the side).
+  const __amdgpu_buffer_rsrc_t ract = rsrc(p.act, p.act_bytes);
+  bool ok = true;
+  float rs[B];
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    rs[i] = 1.0f;
+    for (int k = (i >= p.b ? 0 : K) + tid; k < Kpad; k += NT) xs[i * Kpad + k] = 0.f;
+  }
+  const u32* gsl = o.gain ? reinterpret_cast<const u32*>(o.gain) : nullptr;
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    if (i >= p.b || !ok) continue;
+    float ss = 0.f;
+    auto use = [&](int k, float a, float b, u32 g2) {
+      ss += a * a + b * b;
+      if (gsl) { a *= bf16lo(g2); b *= bf16hi(g2); }
+      xs[i * Kpad + k] = a;
+      xs[i * Kpad + k + 1] = b;
+    };
+    if (o.from_embed) {
+      const uint16_t* e = p.embed + (size_t)st.tok[i] * p.h;
+      for (int k = tid * 2; k < K; k += NT * 2) {
+        const u32 w2 = *reinterpret_cast<const u32*>(e + k);
+        use(k, bf16lo(w2), bf16hi(w2), gsl ? gsl[k >> 1] : 0u);
+      }
+    } else if (!wait_pairs<WBC>(p, st, ract, o.in_w + (u32)i * o.in_stride, K, gsl, use, tid, NT)) {
+      ok = false;
     }
-    __syncthreads();
-    // One thread per batch lane folds the waves' keys into the step's maximum (all lanes'
-    // atomics in flight together), and waits until its atomic has been performed.
-    if (tid < p.b) {
-      u64 k = 0;
-      for (int w = 0; w < NWAVE; ++w) k = wkeys[w * B + tid] > k ? wkeys[w * B + tid] : k;
-      if (k) __hip_atomic_fetch_max(p.amax + tid, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      vm_wait0();
-    }
-    __syncthreads();
-    // The tile that arrives last (all maxima performed) writes the tokens and resets.
-    int* last = reinterpret_cast<int*>(misc + 8);
-    if (tid == 0) {
-      const u32 old = __hip_atomic_fetch_add(p.lm_arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const int is_last = old == (u32)p.n_lm_instr - 1u ? 1 : 0;
-      if (is_last) __hip_atomic_store(p.lm_arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      *last = is_last;
-    }
-    __syncthreads();
-    if (*last && tid < p.b) {
-      const u64 k = __hip_atomic_load(p.amax + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      st.next_ids[tid] = (int32_t)(0xFFFFFFFFu - (u32)(k & 0xFFFFFFFFull));
-      __hip_atomic_store(p.amax + tid, (u64)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (o.gain) {
+      const float wsum = wave_sum(ss);
+      if (lane == 0) mss[wave * B + i] = wsum;
     }
   }
-  __syncthreads();   // LDS is reused by the next instruction
+  // The second chunk's claim was issued before the polls above, which have all returned.
+  if (wave == 0 && pend_slot >= 0) publish();
+  if (__syncthreads_or(!ok)) return false;
+  if (tl && tid == 0) { tl[1] = clock_now(); tl[2] = tl[1]; }
+
+  // 3. Stream every chunk the workgroup takes. Each round consumes the U slots in order and
+  //    refills each after its use; past the last chunk the refills read the zero page.
+  int c_j = 0, c_sg = 0;
+  bool c_live = true;
+  float acc[B];
+#pragma unroll
+  for (int i = 0; i < B; ++i) acc[i] = 0.f;
+  const int kx0 = pt * SP * 128 + (lane & 15) * 8;   // LDS column of segment 0
+  auto consume = [&](const u32x4 w) {
+    if (!c_live) return;
+    if (c_sg < sp_ok) {
+      const int kk = kx0 + c_sg * 128;
+      const float w0 = bf16lo(w.x), w1 = bf16hi(w.x), w2 = bf16lo(w.y), w3 = bf16hi(w.y);
+      const float w4 = bf16lo(w.z), w5 = bf16hi(w.z), w6 = bf16lo(w.w), w7 = bf16hi(w.w);
+#pragma unroll
+      for (int i = 0; i < B; ++i) {
+        const float4 xa = *reinterpret_cast<const float4*>(xs + i * Kpad + kk);
+        const float4 xb = *reinterpret_cast<const float4*>(xs + i * Kpad + kk + 4);
+        float t0 = w0 * xa.x, t1 = w1 * xa.y;
+        t0 = fmaf(w2, xa.z, t0); t1 = fmaf(w3, xa.w, t1);
+        t0 = fmaf(w4, xb.x, t0); t1 = fmaf(w5, xb.y, t1);
+        t0 = fmaf(w6, xb.z, t0); t1 = fmaf(w7, xb.w, t1);
+        acc[i] += t0 + t1;
+      }
+    }
+    c_sg = uni(c_sg + 1);
+    if (c_sg == SP) {
+      // Item done: each 16-lane row sums its weight row; its first lane stores the part.
+#pragma unroll
+      for (int i = 0; i < B; ++i) {
+        const float v = row16_sum(acc[i]);
+        acc[i] = 0.f;
+        if ((lane & 15) == 0) rowacc[((c_j * KP + pt) * nwr + wr) * B + i] = v;
+      }
+      c_sg = 0;
+      c_j = uni(c_j + 1);
+      // the issue cursor passed this boundary U units ago, so the id is published
+      if (uni(chl[c_j]) < 0) c_live = false;
+    }
+  };
+  while (c_live) {
+    if (wave == 0) {
+      if (pend_slot >= 0) publish();
+      if (!exhausted && i_live && i_sg >= claim_from && claimed <= i_j && i_j + 1 < nslot) {
+        if (lane == 0) pend = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        pend_slot = i_j + 1;
+        claimed = i_j + 1;
+      }
+    }
+#pragma unroll
+    for (int sl = 0; sl < U; ++sl) {
+      consume(ring[sl]);
+      issue(ring[sl]);
+    }
+  }
+  __syncthreads();
+  if (tl && tid == 0) tl[3] = clock_now();
+  // Every wave walked the same slots: the consume cursor stopped at the first empty one.
+  const int nused = c_j;
+  if (tl && tid == 0) tl[6] = (u64)nused;
+
+  if (o.gain) {
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+      float t = 0.f;
+      for (int w = 0; w < NWAVE; ++w) t += mss[w * B + i];
+      rs[i] = 1.0f / sqrtf(t / (float)K + p.eps);
+    }
+    if (st.taps && wg == 0) {
+      const int off = (op == FM_OP_QKV) ? p.tap_a : (op == FM_OP_GU ? p.tap_a2 : 0);
+#pragma unroll
+      for (int i = 0; i < B; ++i) {
+        if (i >= p.b) continue;
+        float* t = (op == FM_OP_LM)
+                       ? st.taps + (size_t)p.L * p.b * p.tap_block + (size_t)i * p.h
+                       : st.taps + ((size_t)l * p.b + i) * p.tap_block + off;
+        for (int k = tid; k < K; k += NT) {
+          const float x = o.from_embed
+              ? __uint_as_float((u32)p.embed[(size_t)st.tok[i] * p.h + k] << 16)
+              : __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ract, (o.in_w + (u32)i * o.in_stride + (u32)k) * 8u,
+                                                                      0, CPOL_SC1));
+          t[k] = x * rs[i] * __uint_as_float((u32)o.gain[k] << 16);
+        }
+      }
+    }
+  }
+
+  // 4. Epilogue over the workgroup's rows (chunk slot j, row rl): K-part sums in order,
+  //    residual adds (the residual word is read here, produced two stages ago), tagged
+  //    stores and taps.
+  for (int u = tid; u < nused * Rc && ok; u += NT) {
+    const int j = u / Rc, rl = u - j * Rc;
+    const int r = chl[j] * Rc + rl;
+    if (r >= R) continue;
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+      if (i >= p.b) break;
+      float y = 0.f;
+      for (int q = 0; q < KP; ++q) y += rowacc[((j * KP + q) * nwr + rl) * B + i];
+      if (o.gain) y *= rs[i];
+      float res = 0.f;
+      if (o.has_res) {
+        if (o.res_embed) {
+          res = __uint_as_float((u32)p.embed[(size_t)st.tok[i] * p.h + r] << 16);
+        } else {
+          float ra_, rb_;
+          if (!wait_pair(p, st, ract, o.res_w + (u32)i * o.res_stride + (u32)(r & ~1), ra_, rb_)) { ok = false; break; }
+          res = (r & 1) ? rb_ : ra_;
+        }
+      }
+      switch (op) {
+        case FM_OP_QKV:
+          st_tag(p.act + p.off_qkv + (u32)l * p.st_qkv + (u32)i * nqkv + r, y, st.epoch);
+          if (st.taps) st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_qkv + r] = y;
+          break;
+        case FM_OP_OPROJ: {
+          const float x1 = y + res;
+          st_tag(p.act + p.off_x1 + (u32)l * p.st_x1 + (u32)i * p.h + r, x1, st.epoch);
+          if (st.taps) st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_x1 + r] = x1;
+          break;
+        }
+        default: {  // FM_OP_DOWN
+          const float xr = y + res;
+          st_tag(p.act + p.off_x + (u32)(l + 1) * p.st_x + (u32)i * p.h + r, xr, st.epoch);
+          if (st.taps) {
+            st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_mlp + r] = y;
+            st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_x2 + r] = xr;
+          }
+          break;
+        }
+      }
+    }
+  }
+  if (__syncthreads_or(!ok)) return false;   // also: LDS is reused by the next instruction
   return true;
 }
 

@@ -20,7 +20,7 @@ FM_OP_QKV, FM_OP_ATTN, FM_OP_OPROJ, FM_OP_GU, FM_OP_DOWN, FM_OP_LM = range(1, 7)
 class fm_model_cfg(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_layers", "hidden", "n_heads", "n_kv_heads", "head_dim", "intermediate", "vocab",
-        "qk_norm", "tied_embedding", "batch", "max_ctx", "n_workgroups", "attn_items", "reserved")] + [
+        "qk_norm", "tied_embedding", "batch", "max_ctx", "n_workgroups", "attn_items", "dyn_chunk_kb")] + [
         ("rope_theta", ctypes.c_double), ("rms_eps", ctypes.c_double)]
 
 
@@ -41,7 +41,7 @@ class fm_kv_ptrs(ctypes.Structure):
 class fm_plan_stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_cu", "n_instr", "n_types", "min_instr_per_layer", "n_counters", "attn_items",
-        "attn_max_chunks", "n_stages")] + [
+        "attn_max_chunks", "n_stages", "n_dyn_stages")] + [
         ("max_bytes_per_cu", ctypes.c_double), ("mean_bytes_per_cu", ctypes.c_double),
         ("imbalance", ctypes.c_double)]
 
@@ -99,33 +99,34 @@ def check(status: int, what: str = ""):
         raise FmError(status, what)
 
 
-def make_cfg(cfg: dict, n_workgroups: int = 0, attn_items: int = 0) -> fm_model_cfg:
+def make_cfg(cfg: dict, n_workgroups: int = 0, attn_items: int = 0, dyn_chunk_kb: int = 0) -> fm_model_cfg:
     c = fm_model_cfg()
     for n in ("n_layers", "hidden", "n_heads", "n_kv_heads", "head_dim", "intermediate", "vocab",
               "qk_norm", "tied_embedding", "batch", "max_ctx"):
         setattr(c, n, int(cfg[n]))
     c.n_workgroups = int(n_workgroups)
     c.attn_items = int(attn_items)
-    c.reserved = 0
+    c.dyn_chunk_kb = int(dyn_chunk_kb)
     c.rope_theta = float(cfg["rope_theta"])
     c.rms_eps = float(cfg["rms_eps"])
     return c
 
 
-def plan_query(cfg: dict, n_cu: int, attn_items: int = 0) -> fm_plan_stats:
+def plan_query(cfg: dict, n_cu: int, attn_items: int = 0, dyn_chunk_kb: int = 0) -> fm_plan_stats:
     s = fm_plan_stats()
-    check(load().fm_plan_query(ctypes.byref(make_cfg(cfg, attn_items=attn_items)), int(n_cu), ctypes.byref(s)),
+    check(load().fm_plan_query(ctypes.byref(make_cfg(cfg, attn_items=attn_items, dyn_chunk_kb=dyn_chunk_kb)),
+                               int(n_cu), ctypes.byref(s)),
           "fm_plan_query")
     return s
 
 
-def plan_export(cfg: dict, n_cu: int, attn_items: int = 0):
+def plan_export(cfg: dict, n_cu: int, attn_items: int = 0, dyn_chunk_kb: int = 0):
     """Returns (qoff int32[n_cu+1], instrs int32[n][4]) as numpy arrays."""
     import numpy as np
-    s = plan_query(cfg, n_cu, attn_items)
+    s = plan_query(cfg, n_cu, attn_items, dyn_chunk_kb)
     qoff = np.zeros(n_cu + 1, dtype=np.int32)
     ins = np.zeros((s.n_instr, 4), dtype=np.int32)
-    check(load().fm_plan_export(ctypes.byref(make_cfg(cfg, attn_items=attn_items)), int(n_cu),
+    check(load().fm_plan_export(ctypes.byref(make_cfg(cfg, attn_items=attn_items, dyn_chunk_kb=dyn_chunk_kb)), int(n_cu),
                                 qoff.ctypes.data, qoff.size, ins.ctypes.data, ins.size), "fm_plan_export")
     return qoff, ins
 
@@ -142,7 +143,8 @@ class Decoder:
     The tensors must stay alive (this object keeps references).
     """
 
-    def __init__(self, cfg: dict, weights: dict, kcache, vcache, n_workgroups: int = 0, attn_items: int = 0):
+    def __init__(self, cfg: dict, weights: dict, kcache, vcache, n_workgroups: int = 0, attn_items: int = 0,
+                 dyn_chunk_kb: int = 0):
         import torch
         self.cfg = dict(cfg)
         self._keep = [weights, kcache, vcache]
@@ -165,7 +167,7 @@ class Decoder:
         kp = (ctypes.c_void_p * L)(*[t.data_ptr() for t in kcache])
         vp = (ctypes.c_void_p * L)(*[t.data_ptr() for t in vcache])
         kv = fm_kv_ptrs(ctypes.cast(kp, ctypes.POINTER(ctypes.c_void_p)), ctypes.cast(vp, ctypes.POINTER(ctypes.c_void_p)))
-        self._c = make_cfg(cfg, n_workgroups, attn_items)
+        self._c = make_cfg(cfg, n_workgroups, attn_items, dyn_chunk_kb)
         self._layers, self._w, self._kp, self._vp, self._kv = layers, w, kp, vp, kv
         h = ctypes.c_void_p()
         check(load().fm_create(ctypes.byref(self._c), ctypes.byref(w), ctypes.byref(kv), ctypes.byref(h)), "fm_create")

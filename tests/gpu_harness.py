@@ -108,7 +108,7 @@ class Pair:
     """A workload loaded on both sides."""
 
     def __init__(self, name, steps=None, gains="ones", poison=False, n_workgroups=0, attn_items=0, taps=True,
-                 cfg_override=None, device="cpu"):
+                 cfg_override=None, device="cpu", dyn_chunk_kb=0):
         """``device``: where the seeded inputs are drawn ("cuda" for the full-size shapes)."""
         from oracle.oracle import Oracle
         from paper_2609_12379_amd.fm import Decoder, tap_count
@@ -125,7 +125,8 @@ class Pair:
         self.wdev = to_dev(self.wl.weights)
         self.kc_d = [t.cuda() for t in self.wl.kcache]
         self.vc_d = [t.cuda() for t in self.wl.vcache]
-        self.dec = Decoder(cfg, self.wdev, self.kc_d, self.vc_d, n_workgroups=n_workgroups, attn_items=attn_items)
+        self.dec = Decoder(cfg, self.wdev, self.kc_d, self.vc_d, n_workgroups=n_workgroups, attn_items=attn_items,
+                           dyn_chunk_kb=dyn_chunk_kb)
         self.taps = None
         if taps:
             self.taps = torch.zeros(tap_count(cfg), dtype=torch.float32, device="cuda")

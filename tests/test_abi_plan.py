@@ -96,14 +96,14 @@ def test_cfg_validation(fm, field, value, status):
     assert got == status, f"{field}={value}: status {got}, expected {status}"
 
 
-def test_cfg_validation_group_and_reserved(fm):
+def test_cfg_validation_group_and_tuning(fm):
     L = fm.load()
     s = fm.fm_plan_stats()
     cfg = _with_ctx(get_config("toy-gpu"))
     cfg.update(n_heads=36, n_kv_heads=4)                      # G = 9 > 8
     assert L.fm_plan_query(ctypes.byref(fm.make_cfg(cfg)), 64, ctypes.byref(s)) == 2
     c = fm.make_cfg(_with_ctx(get_config("toy-gpu")))
-    c.reserved = 1
+    c.dyn_chunk_kb = -2
     assert L.fm_plan_query(ctypes.byref(c), 64, ctypes.byref(s)) == 1
     c = fm.make_cfg(_with_ctx(get_config("toy-gpu")))
     c.rope_theta = 0.0
@@ -154,6 +154,30 @@ def _order_key(op, layer, L):
     return (L, 0) if op == OP_LM else (layer, STAGE[op])
 
 
+POOLS = 8
+
+
+def dyn_chunk_rows(n_rows, rc, kp, slots, nwg):
+    """Row ranges of a stage in dynamic chunks, rebuilt from its record as the header
+    describes it, after checking what the kernel relies on: every pool holds at least one
+    chunk per workgroup (each takes its own one) and at most `slots` per workgroup (so the
+    pool is always drained, whoever takes its chunks)."""
+    assert rc >= 1 and kp in (1, 2, 4, 8) and slots >= 2
+    nch = -(-n_rows // rc)
+    np_ = min(POOLS, nwg)
+    out = []
+    start = 0
+    for x in range(np_):
+        nwx = len(range(x, nwg, np_))
+        c0 = nch * start // nwg
+        c1 = nch * (start + nwx) // nwg
+        assert nwx <= c1 - c0 <= nwx * slots, (x, nwx, c0, c1, slots)
+        for c in range(c0, c1):
+            out.append((c * rc, min(n_rows, (c + 1) * rc)))
+        start += nwx
+    return out
+
+
 def check_plan(cfg, nwg, fm):
     s = fm.plan_query(cfg, nwg)
     qoff, ins = fm.plan_export(cfg, nwg)
@@ -163,9 +187,12 @@ def check_plan(cfg, nwg, fm):
     assert P > nkv * b and s.attn_max_chunks == (P - nkv * b) // nkv + 1
     rows = _gemv_rows(cfg)
     cover = {}
+    dyn = {}
     for op, layer, a, bb in ins:
         op, layer = int(op), int(layer)
-        if op in rows:
+        if op in rows and a < 0:
+            dyn.setdefault((op, layer), []).append((int(-a), int(bb)))
+        elif op in rows:
             assert 0 <= a < bb <= rows[op], (op, layer, a, bb)
             cover.setdefault((op, layer), []).append((int(a), int(bb)))
         elif op == OP_ATTN:
@@ -173,6 +200,13 @@ def check_plan(cfg, nwg, fm):
             cover.setdefault((op, layer), []).append((int(a), int(a) + 1))
         else:
             raise AssertionError(f"unknown op {op}")
+    # stages in dynamic chunks: every workgroup holds the same record, and the pools' chunk
+    # ranges cover the rows exactly once
+    for (op, l), recs in dyn.items():
+        assert len(recs) == nwg and len(set(recs)) == 1, (op, l)
+        rc, packed = recs[0]
+        cover.setdefault((op, l), []).extend(dyn_chunk_rows(rows[op], rc, packed & 255, packed >> 8, nwg))
+    assert s.n_dyn_stages == len(dyn)
     # every row / item / group exactly once
     for l in range(L):
         for op, n in ((OP_QKV, rows[OP_QKV]), (OP_OPROJ, rows[OP_OPROJ]), (OP_GU, rows[OP_GU]),
@@ -196,7 +230,8 @@ def check_plan(cfg, nwg, fm):
     for w in range(nwg):
         for o, l, a, bb in ins[qoff[w]:qoff[w + 1]]:
             if int(o) in cols:
-                per[w] += (bb - a) * cols[int(o)] * 2
+                # a dynamic stage counts its mean share
+                per[w] += (rows[int(o)] / nwg if a < 0 else bb - a) * cols[int(o)] * 2
     assert abs(per.max() - s.max_bytes_per_cu) <= 1e-6 * per.max()
     assert abs(per.mean() - s.mean_bytes_per_cu) <= 1e-6 * per.mean()
     return s, qoff, ins

@@ -18,11 +18,14 @@ def _need_gpu():
         pytest.skip("needs a GPU")
 
 
-def _one_call(name, ctx):
+def _one_call(name, ctx, n_workgroups=0):
     from tests.gpu_harness import Pair, check_greedy, rel_l2, MAX_ABS, REL_L2
-    print(f"case {name} ctx={ctx}", flush=True)
-    a = Pair(name, gains="uniform", taps=False, cfg_override={"ctx": ctx})
-    b = Pair(name, gains="uniform", taps=False, cfg_override={"ctx": ctx})
+    print(f"case {name} ctx={ctx} nwg={n_workgroups}", flush=True)
+    a = Pair(name, gains="uniform", taps=False, cfg_override={"ctx": ctx}, n_workgroups=n_workgroups)
+    b = Pair(name, gains="uniform", taps=False, cfg_override={"ctx": ctx}, n_workgroups=n_workgroups)
+    if n_workgroups:
+        from paper_2609_12379_amd.fm import plan_query
+        assert plan_query(a.cfg, n_workgroups).n_dyn_stages > 0
     need = b.dec.noalloc_scratch_bytes()
     assert 0 < need <= (64 << 20), need
     S = a.wl.S
@@ -52,6 +55,15 @@ def _one_call(name, ctx):
 def test_noalloc_step_matches_the_allocating_step():
     big = _one_call("mini-qwen3-b4", (200, 900))
     small = _one_call("toy-gpu", (5, 12))
+    assert small < big
+
+
+def test_noalloc_step_with_dynamic_chunks():
+    """Stages in dynamically claimed chunks keep their claim counters in the fixed scratch too:
+    two handles of different depth in a row (different counter layouts), each cleared before
+    its step."""
+    big = _one_call("mini-qwen3", (300, 300), n_workgroups=7)
+    small = _one_call("mini-llama3", (40, 90), n_workgroups=13)
     assert small < big
 
 
