@@ -215,13 +215,15 @@ __device__ __forceinline__ u32 ordered(float f) {
 // flight exactly); lanes with nothing to load read a zeroed page instead. The last round
 // issues none.
 //
-// Batched tiles (B >= 4) run the products on the matrix cores instead (a skinny GEMM):
-// a unit is then 16 weight rows x 32 columns, loaded in the A-operand layout of
+// Batch-8 tiles run the products on the matrix cores instead (a skinny GEMM): a unit is
+// then 16 weight rows x 32 columns, loaded in the A-operand layout of
 // v_mfma_f32_16x16x32_bf16 (lane l: row l % 16, columns 8 (l / 16) .. + 8, still one 16 B
-// load per lane). The B operand is the activation slab: each fp32 value x is split into
-// bf16 hi = rne(x) and lo = rne(x - hi), and both halves go through the matrix core into
-// the same fp32 accumulator, so the product keeps about 16 bits of the activation's
-// mantissa. Lanes 16 .. of the B operand's 16 columns (batch lanes past B) are zero.
+// load per lane). The B operand is the activation slab: each fp32 value x is split into three
+// bf16 planes hi = rne(x), mid = rne(x - hi), lo = rne(x - hi - mid), and all three go
+// through the matrix core into the same fp32 accumulator, so the product keeps about 24 bits
+// of the activation's mantissa. Lanes 16 .. of the B operand's 16 columns (batch lanes past B)
+// are zero. (At batch 4 the VALU tiles measured faster on MI355X; at batch 8 the matrix
+// cores.)
 
 struct GemvGeom {
   int K, Ks, nslab;           // columns, slab width, slabs
@@ -416,7 +418,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
   // Geometry (all wave-uniform).
   GemvGeom g;
   g.K = K;
-  constexpr bool MF = (B >= 4);           // matrix-core tiles for batched steps
+  constexpr bool MF = (B >= 8);           // matrix-core tiles for batch 8
   using US = UnitShape<MF>;
   constexpr int XSF = xslab_floats<B>();
   {

@@ -50,6 +50,24 @@ def test_full_size_parity(name, poison):
 
 @pytest.mark.gpu
 @pytest.mark.timeout(900)
+@pytest.mark.parametrize("S", [64, 4096])
+def test_context_sweep_endpoints_qwen3_8b_b1(S):
+    """The one kernel serves every context up to the arena's bound (the paper compiles one
+    kernel per context bin, Sec. 5.3): the Qwen3-8B b1 shape at both ends of the context
+    sweep, two steps each against the oracle."""
+    name = "qwen3-8b-b1"
+    print(f"[{name} S={S}] drawing inputs on the device", flush=True)
+    pair = Pair(name, steps=2, device="cuda", cfg_override={"ctx": (S, S)})
+    assert pair.wl.S == [S]
+    try:
+        reps = pair.run(2, log=_log(f"{name} S={S}"))
+    finally:
+        pair.close()
+    assert len(reps) == 2
+
+
+@pytest.mark.gpu
+@pytest.mark.timeout(900)
 def test_bench_loop_llama3_2_1b():
     """The benchmark's loop: step t reads step t-1's next_ids buffer on the device."""
     name, K = "llama3.2-1b", 6

@@ -1,7 +1,7 @@
 """The dependency gate of Sec. 4.1, measured from the per-instruction timeline.
 
-On the Llama-3.2-1B-shaped workload (b1, context 2048), in the launch configuration the
-benchmark times:
+On the Llama-3.2-1B-shaped workload (b1, context 2048) and the Llama-2-13B b1 workload
+(context 2048), in the launch configuration the benchmark times:
   * busy_frac: the instructions' spans (start to end, waits included) over
     workgroups x step time, at least 0.85;
   * tail_spread: first to last workgroup finish over the step time, at most 0.05;
@@ -19,11 +19,13 @@ import torch
 
 @pytest.mark.gpu
 @pytest.mark.timeout(600)
-def test_dependency_gate_from_timeline():
+@pytest.mark.parametrize("name", ["llama3.2-1b", "llama2-13b-b1"])
+def test_dependency_gate_from_timeline(name):
     from synthetic import get_config, make_workload
     from paper_2609_12379_amd.fm import Decoder, plan_export
 
-    cfg0 = get_config("llama3.2-1b")
+    print(f"case {name}", flush=True)
+    cfg0 = get_config(name)
     wl = make_workload(cfg0, steps=24, device="cuda")
     cfg = wl.cfg
     wd = {k: v for k, v in wl.weights.items() if k != "layers" and v is not None}
