@@ -47,7 +47,7 @@ constexpr int NSW = NWAVE - NCTL;
 //   attention items: [merger's partials, kMergeFloats] ... [item scratch ATT][MISC].
 // Matrix-core (batched) tiles need fewer row sums and a larger slab.
 constexpr int LDS_FLOATS = 40448;
-constexpr int MISC_FLOATS = 1024;   // block reductions, argmax keys
+constexpr int MISC_FLOATS = 1024;   // block reductions, argmax keys, chunk ids; timeline marks in the last 24
 constexpr int RESID_FLOATS = 2048;  // residual rows staged for the epilogue
 constexpr int ATT_FLOATS = 9600;    // q heads, k, v and per-wave partials of one item (G <= 8, d <= 128)
 template <int B> constexpr int rowacc_floats() { return B >= 4 ? 4096 : 8192; }
@@ -201,6 +201,11 @@ __device__ __forceinline__ u64 wave_max_u64(u64 k) {
 }
 
 __device__ __forceinline__ u64 clock_now() { return wall_clock64(); }
+
+// Instruction timeline marks are kept in LDS while an instruction runs (and written to memory
+// when it ends): a store to memory in the middle of an operator would make its next full wait
+// for loads also wait for the store's acknowledgement.
+typedef __attribute__((address_space(3))) u64 tl_t;
 
 // Watchdog bound on any single wait (wall clock runs at 100 MHz on MI355X): 2 s.
 constexpr u64 WAIT_TICKS = 200000000ull;

@@ -49,7 +49,8 @@ __global__ __launch_bounds__(NT, 1) void step_kernel(const Params* __restrict__ 
     CParams& P = *pp;
     const int32_t* ins = P.instrs + 4 * (size_t)q;
     const int op = ins[0];
-    u64* tl = st.timeline ? st.timeline + 8 * (size_t)q : nullptr;
+    u64* tg = st.timeline ? st.timeline + 8 * (size_t)q : nullptr;
+    tl_t* tl = tg ? (tl_t*)(__attribute__((address_space(3))) float*)(smem + LDS_FLOATS - 24) : nullptr;   // 8 marks
     if (tl && tid == 0) { tl[0] = clock_now(); tl[1] = 0; tl[2] = 0; tl[3] = 0; tl[5] = (u64)wg; tl[6] = 0; tl[7] = 0; }
     bool ok = true;
     if (op == FM_OP_ATTN) {
@@ -68,7 +69,11 @@ __global__ __launch_bounds__(NT, 1) void step_kernel(const Params* __restrict__ 
       ok = op_gemv<B, 1>(P, st, ins, smem, tid, lane, wave, tl);
     }
     if (!ok) return;
-    if (tl && tid == 0) tl[4] = clock_now();
+    if (tl && tid == 0) {
+      tl[4] = clock_now();
+#pragma unroll
+      for (int k = 0; k < 8; ++k) tg[k] = tl[k];
+    }
   }
 }
 

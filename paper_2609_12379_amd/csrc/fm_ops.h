@@ -313,6 +313,8 @@ struct GemvOperand {
   const uint16_t* m0 = nullptr;     // matrices: QKV uses m0..m2 (W_q, W_k, W_v), GU m0, m1
   const uint16_t* m1 = nullptr;
   const uint16_t* m2 = nullptr;
+  u64* out = nullptr;               // tagged output of lane 0 (not the LM head)
+  u32 out_stride = 0;               // words per batch lane
 };
 
 __device__ __forceinline__ GemvOperand gemv_operand(CParams& p, int op, int l) {
@@ -324,22 +326,26 @@ __device__ __forceinline__ GemvOperand gemv_operand(CParams& p, int op, int l) {
       o.K = p.h; o.rows = nq + 2 * nk; o.sidx = 4 * l; o.gain = Lw->attn_norm;
       if (l == 0) o.from_embed = true; else { o.in_w = p.off_x + (u32)l * p.st_x; o.in_stride = p.h; }
       o.m0 = Lw->wq; o.m1 = Lw->wk; o.m2 = Lw->wv;
+      o.out = p.act + p.off_qkv + (u32)l * p.st_qkv; o.out_stride = (u32)(nq + 2 * nk);
       break;
     case FM_OP_OPROJ:
       o.K = nq; o.rows = p.h; o.sidx = 4 * l + 1; o.in_w = p.off_o + (u32)l * p.st_o; o.in_stride = nq;
       o.has_res = true;
       if (l == 0) o.res_embed = true; else { o.res_w = p.off_x + (u32)l * p.st_x; o.res_stride = p.h; }
       o.m0 = Lw->wo;
+      o.out = p.act + p.off_x1 + (u32)l * p.st_x1; o.out_stride = (u32)p.h;
       break;
     case FM_OP_GU:
       o.K = p.h; o.rows = p.inter; o.sidx = 4 * l + 2; o.gain = Lw->mlp_norm;
       o.in_w = p.off_x1 + (u32)l * p.st_x1; o.in_stride = p.h;
       o.m0 = Lw->wg; o.m1 = Lw->wu;
+      o.out = p.act + p.off_m + (u32)l * p.st_m; o.out_stride = (u32)p.inter;
       break;
     case FM_OP_DOWN:
       o.K = p.inter; o.rows = p.h; o.sidx = 4 * l + 3; o.in_w = p.off_m + (u32)l * p.st_m; o.in_stride = p.inter;
       o.has_res = true; o.res_w = p.off_x1 + (u32)l * p.st_x1; o.res_stride = p.h;
       o.m0 = Lw->wd;
+      o.out = p.act + p.off_x + (u32)(l + 1) * p.st_x; o.out_stride = (u32)p.h;
       break;
     default:  // FM_OP_LM
       o.K = p.h; o.rows = p.V; o.sidx = 4 * p.L; o.gain = p.final_norm;
@@ -401,10 +407,10 @@ __device__ __forceinline__ void lm_finish(CParams& p, const Step& st, const u64 
 
 template <int B, int NW>
 __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_t* ins, float* smem, int tid,
-                                        int lane, int wave, u64* tl) {
+                                        int lane, int wave, tl_t* tl) {
   const int op = uni(ins[0]), l = uni(ins[1]), ra = uni(ins[2]), rb = uni(ins[3]);
   const int nr = rb - ra;
-  const int nq = p.nh * p.d, nk = p.nkv * p.d, nqkv = nq + 2 * nk;
+  const int nq = p.nh * p.d, nk = p.nkv * p.d;
 
   // Operator geometry.
   const GemvOperand opd = gemv_operand(p, op, l);
@@ -710,10 +716,13 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
 
   // 4. Epilogue, one output row per thread: K-part sums in order, residual adds, SiLU * up,
   //    tagged stores, taps, logits; the LM head also folds its rows into one packed argmax
-  //    key per lane.
+  //    key per lane. The output's address was resolved with the operator, so nothing here
+  //    waits on parameter loads.
   u64 key[B];
 #pragma unroll
   for (int i = 0; i < B; ++i) key[i] = 0;
+  u64* const out = opd.out;
+  const u32 ost = opd.out_stride, epoch = st.epoch;
   for (int rl = tid; rl < nr; rl += NT) {
     const int r = ra + rl;
 #pragma unroll
@@ -730,21 +739,21 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
       }
       switch (op) {
         case FM_OP_QKV:
-          st_tag(p.act + p.off_qkv + (u32)l * p.st_qkv + (u32)i * nqkv + r, y, st.epoch);
+          st_tag(out + (u32)i * ost + r, y, epoch);
           if (st.taps) st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_qkv + r] = y;
           break;
         case FM_OP_OPROJ: {
           const float x1 = y + resid[i * nr + rl];
-          st_tag(p.act + p.off_x1 + (u32)l * p.st_x1 + (u32)i * p.h + r, x1, st.epoch);
+          st_tag(out + (u32)i * ost + r, x1, epoch);
           if (st.taps) st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_x1 + r] = x1;
           break;
         }
         case FM_OP_GU:
-          st_tag(p.act + p.off_m + (u32)l * p.st_m + (u32)i * p.inter + r, silu(y) * up, st.epoch);
+          st_tag(out + (u32)i * ost + r, silu(y) * up, epoch);
           break;
         case FM_OP_DOWN: {
           const float xr = y + resid[i * nr + rl];
-          st_tag(p.act + p.off_x + (u32)(l + 1) * p.st_x + (u32)i * p.h + r, xr, st.epoch);
+          st_tag(out + (u32)i * ost + r, xr, epoch);
           if (st.taps) {
             st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_mlp + r] = y;
             st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_x2 + r] = xr;
@@ -794,13 +803,13 @@ typedef __attribute__((address_space(3))) volatile int lds_int;
 
 template <int B>
 __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const int32_t* ins, float* smem, int tid,
-                                            int lane, int wave, u64* tl) {
+                                            int lane, int wave, tl_t* tl) {
   static_assert(B <= 2 && NCTL == 0, "dynamic chunks run VALU tiles streamed by every wave");
   constexpr int U = FM_RING;
   constexpr int UNKNOWN = -2, END = -1;
   const int op = uni(ins[0]), l = uni(ins[1]);
   const int Rc = uni(-ins[2]), KP = uni(ins[3] & 0xff), nslot = uni(ins[3] >> 8);
-  const int nq = p.nh * p.d, nk = p.nkv * p.d, nqkv = nq + 2 * nk;
+  const int nq = p.nh * p.d, nk = p.nkv * p.d;
   const GemvOperand o = gemv_operand(p, op, l);
   const int K = o.K, R = o.rows;
   const int Kpad = uni((K + 127) & ~127), nseg = uni(Kpad / 128);
@@ -1052,6 +1061,8 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
   // 4. Epilogue over the workgroup's rows (chunk slot j, row rl): K-part sums in order,
   //    residual adds (the residual word is read here, produced two stages ago), tagged
   //    stores and taps.
+  u64* const out = o.out;
+  const u32 ost = o.out_stride, epoch = st.epoch;
   for (int u = tid; u < nused * Rc && ok; u += NT) {
     const int j = u / Rc, rl = u - j * Rc;
     const int r = chl[j] * Rc + rl;
@@ -1074,18 +1085,18 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
       }
       switch (op) {
         case FM_OP_QKV:
-          st_tag(p.act + p.off_qkv + (u32)l * p.st_qkv + (u32)i * nqkv + r, y, st.epoch);
+          st_tag(out + (u32)i * ost + r, y, epoch);
           if (st.taps) st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_qkv + r] = y;
           break;
         case FM_OP_OPROJ: {
           const float x1 = y + res;
-          st_tag(p.act + p.off_x1 + (u32)l * p.st_x1 + (u32)i * p.h + r, x1, st.epoch);
+          st_tag(out + (u32)i * ost + r, x1, epoch);
           if (st.taps) st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_x1 + r] = x1;
           break;
         }
         default: {  // FM_OP_DOWN
           const float xr = y + res;
-          st_tag(p.act + p.off_x + (u32)(l + 1) * p.st_x + (u32)i * p.h + r, xr, st.epoch);
+          st_tag(out + (u32)i * ost + r, xr, epoch);
           if (st.taps) {
             st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_mlp + r] = y;
             st.taps[((size_t)l * p.b + i) * p.tap_block + p.tap_x2 + r] = xr;
@@ -1235,24 +1246,31 @@ __device__ __forceinline__ bool merge_group(CParams& p, const Step& st, int l, i
   for (int u = tid; u < G * D; u += NT) {
     const int h = u / D, e = u % D;
     const float* src = cp + h * per_head;
-    // Grouped-query kernels unroll the chunk loops so that the LDS reads of several chunks
-    // are in flight together (measured faster there, not with one head per group); the sums
-    // run in chunk order either way.
+    // The chunks in batches of 8: a batch's reads are issued together (indices past the last
+    // chunk read the last chunk again and are dropped by a select), then used in chunk order.
     float M = -INFINITY, den = 0.f, num = 0.f;
-    auto add_chunk = [&](int cc) {
-      const float* pc = src + cc * row;
-      const float f = exp2f(pc[D] - M);
-      den += f * pc[D + 1];
-      num += f * pc[e];
-    };
-    if constexpr (GT >= 2) {
-#pragma unroll 8
-      for (int cc = 0; cc < nc; ++cc) M = fmaxf(M, src[cc * row + D]);
-#pragma unroll 8
-      for (int cc = 0; cc < nc; ++cc) add_chunk(cc);
-    } else {
-      for (int cc = 0; cc < nc; ++cc) M = fmaxf(M, src[cc * row + D]);
-      for (int cc = 0; cc < nc; ++cc) add_chunk(cc);
+    for (int c0 = 0; c0 < nc; c0 += 8) {
+      float mv[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) mv[k] = src[min(c0 + k, nc - 1) * row + D];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) M = fmaxf(M, c0 + k < nc ? mv[k] : -INFINITY);
+    }
+    for (int c0 = 0; c0 < nc; c0 += 8) {
+      float mv[8], lv[8], ov[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float* pc = src + min(c0 + k, nc - 1) * row;
+        mv[k] = pc[D];
+        lv[k] = pc[D + 1];
+        ov[k] = pc[e];
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float f = c0 + k < nc ? exp2f(mv[k] - M) : 0.f;
+        den += f * lv[k];
+        num += f * ov[k];
+      }
     }
     const float o = num / den;
     st_tag(p.act + obase + (u32)((g * G + h) * D + e), o, st.epoch);
@@ -1263,7 +1281,7 @@ __device__ __forceinline__ bool merge_group(CParams& p, const Step& st, int l, i
 
 template <int D, int GT>
 __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_t* ins, float* smem, int tid,
-                                        int lane, int wave, u64* tl) {
+                                        int lane, int wave, tl_t* tl) {
   // Grouped-query kernels with d = 64 (GT >= 2) run the scores and the weighted V sums on the
   // matrix cores in tiles of 16 slots per wave (pass width 128). At d = 128 the matrix-core
   // tiles measured slower on the Qwen3-0.6B shape and barely faster elsewhere, so those
@@ -1545,11 +1563,18 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
       if ((lane >> 4) == 0) { w[D] = m; w[D + 1] = ls; }
     }
   } else {
+    // q of the group's heads for this lane's 8 dims: two 16-byte LDS reads per head, all in
+    // flight together (heads past G read the buffer's unused rows and are zeroed by the
+    // select, not by a branch around the read).
     float qr[GT][8];
   #pragma unroll
-    for (int h = 0; h < GT; ++h)
+    for (int h = 0; h < GT; ++h) {
+      const float4 a = *reinterpret_cast<const float4*>(qs + h * D + de);
+      const float4 c = *reinterpret_cast<const float4*>(qs + h * D + de + 4);
+      const float v[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
   #pragma unroll
-      for (int e = 0; e < 8; ++e) qr[h][e] = (h < G) ? qs[h * D + de + e] * p.q_scale : 0.f;
+      for (int e = 0; e < 8; ++e) qr[h][e] = (h < G) ? v[e] * p.q_scale : 0.f;
+    }
     float m[GT], ls[GT], acc[GT][8];
   #pragma unroll
     for (int h = 0; h < GT; ++h) {
@@ -1668,20 +1693,24 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
   const int row = D + 2;
   for (int u = tid; u < G * row; u += NT) {
     const int h = u / row, e = u % row;
-    float M = -INFINITY;
-    for (int w = 0; w < NWAVE; ++w) M = fmaxf(M, wst[(w * GT + h) * row + D]);
-    float val;
-    if (e == D) {
-      val = M;
-    } else {
-      float A = 0.f;
-      for (int w = 0; w < NWAVE; ++w) {
-        const float* ws = wst + (w * GT + h) * row;
-        const float f = (ws[D] == -INFINITY) ? 0.f : exp2f(ws[D] - M);
-        A += ws[e] * f;           // e == D + 1 sums the softmax denominators
-      }
-      val = A;
+    // Every wave's maximum and value first (all reads in flight together), then the sum in
+    // wave order; an empty wave (maximum -inf) contributes 0 through a select, not a branch.
+    float mw[NWAVE], vw[NWAVE];
+#pragma unroll
+    for (int w = 0; w < NWAVE; ++w) {
+      mw[w] = wst[(w * GT + h) * row + D];
+      vw[w] = wst[(w * GT + h) * row + e];
     }
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NWAVE; ++w) M = fmaxf(M, mw[w]);
+    float A = 0.f;
+#pragma unroll
+    for (int w = 0; w < NWAVE; ++w) {
+      const float f = exp2f(mw[w] - M);
+      A += vw[w] * (mw[w] == -INFINITY ? 0.f : f);   // e == D + 1 sums the softmax denominators
+    }
+    const float val = (e == D) ? M : A;
     if (is_last) {
       cp[(h * nc + (nc - 1)) * row + e] = val;
     } else {
