@@ -83,31 +83,65 @@ __device__ __forceinline__ bool repoll(CParams& p, const Step& st, __amdgpu_buff
 // Polls n (even) tagged words from word w0 on, pairs k = t*2 + j*nthr*2 as wait_copy_t does,
 // and hands each pair, once current, to use(k, a, b, side) in index order. side is the u32
 // at side[k / 2] (a pair of bf16 gains), loaded with the poll; 0 when side is null.
+// One batch of pair loads per thread (pairs k = k0 + j * nthr * 2, j < WBT), with their side
+// words.
+template <int WBT>
+struct PairBatch {
+  u32x4 v[WBT];
+  u32 w[WBT], sv[WBT];
+};
+
+template <int WBT>
+__device__ __forceinline__ void issue_pairs(__amdgpu_buffer_rsrc_t ra, u32 w0, int n, const u32* side, int k0,
+                                            int nthr, PairBatch<WBT>& b) {
+#pragma unroll
+  for (int j = 0; j < WBT; ++j) {
+    const int k = k0 + j * nthr * 2;
+    b.w[j] = (k < n) ? w0 + (u32)k : 0x1FFFFFFEu;
+    b.v[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, (k < n) ? b.w[j] * 8u : 0xFFFFFFF0u, 0, CPOL_SC1);
+    b.sv[j] = (side && k < n) ? side[k >> 1] : 0u;
+  }
+}
+
+template <int WBT, class Use>
+__device__ __forceinline__ bool finish_pairs(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, int n, Use use,
+                                             int k0, int nthr, PairBatch<WBT>& b) {
+  u32 pend = 0;
+#pragma unroll
+  for (int j = 0; j < WBT; ++j) {
+    const int k = k0 + j * nthr * 2;
+    if (k < n && (b.v[j].y != st.epoch || b.v[j].w != st.epoch)) pend |= 1u << j;
+  }
+  if (pend && !repoll<WBT>(p, st, ra, b.w, b.v, pend)) return false;
+#pragma unroll
+  for (int j = 0; j < WBT; ++j) {
+    const int k = k0 + j * nthr * 2;
+    if (k < n) use(k, __uint_as_float(b.v[j].x), __uint_as_float(b.v[j].z), b.sv[j]);
+  }
+  return true;
+}
+
+// Pairs per thread of an input's early poll batch, issued ahead of the weight prefetch: with 512
+// threads a vector of up to 4096 values, and few registers held across the prefetch. Longer
+// inputs are polled after the prefetch in full batches as before (split, they would cost an
+// extra round trip).
+constexpr int WBF = 4;
+
+// first: the caller's first WBF pairs (k0 = t * 2), already issued with the same arguments, or
+// null.
 template <int WBT, class Use>
 __device__ __forceinline__ bool wait_pairs(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, u32 w0, int n,
-                                           const u32* side, Use use, int t, int nthr) {
-  for (int k0 = t * 2; k0 < n; k0 += nthr * 2 * WBT) {
-    u32x4 v[WBT];
-    u32 w[WBT], sv[WBT];
-    u32 pend = 0;
-#pragma unroll
-    for (int j = 0; j < WBT; ++j) {
-      const int k = k0 + j * nthr * 2;
-      w[j] = (k < n) ? w0 + (u32)k : 0x1FFFFFFEu;
-      v[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, (k < n) ? w[j] * 8u : 0xFFFFFFF0u, 0, CPOL_SC1);
-      sv[j] = (side && k < n) ? side[k >> 1] : 0u;
-    }
-#pragma unroll
-    for (int j = 0; j < WBT; ++j) {
-      const int k = k0 + j * nthr * 2;
-      if (k < n && (v[j].y != st.epoch || v[j].w != st.epoch)) pend |= 1u << j;
-    }
-    if (pend && !repoll<WBT>(p, st, ra, w, v, pend)) return false;
-#pragma unroll
-    for (int j = 0; j < WBT; ++j) {
-      const int k = k0 + j * nthr * 2;
-      if (k < n) use(k, __uint_as_float(v[j].x), __uint_as_float(v[j].z), sv[j]);
-    }
+                                           const u32* side, Use use, int t, int nthr,
+                                           PairBatch<WBF>* first = nullptr) {
+  int k0 = t * 2;
+  if (first) {
+    if (!finish_pairs<WBF>(p, st, ra, n, use, k0, nthr, *first)) return false;
+    k0 += nthr * 2 * WBF;
+  }
+  for (; k0 < n; k0 += nthr * 2 * WBT) {
+    PairBatch<WBT> b;
+    issue_pairs<WBT>(ra, w0, n, side, k0, nthr, b);
+    if (!finish_pairs<WBT>(p, st, ra, n, use, k0, nthr, b)) return false;
   }
   return true;
 }
@@ -484,6 +518,17 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
 #pragma unroll
     for (int sl = 0; sl < U; ++sl) refill(sl);
   };
+  // The first batch of input polls goes out before the weight prefetch: a wave's loads
+  // return in issue order, so a poll issued behind the prefetch could not report a ready
+  // input before the prefetch had landed.
+  // (Not on the matrix-core tiles: their registers are taken by the planes' staging.)
+  PairBatch<WBF> pre;
+  const bool early = !MF && !from_embed && p.b > 0 && (NCTL == 0 || wave >= NSW) &&
+                     min(g.Ks, K) <= (NCTL ? NCTL * 64 : NT) * 2 * WBF;
+  if constexpr (!MF)
+    if (early)
+      issue_pairs<WBF>(ract, in_w, min(g.Ks, K), gain ? reinterpret_cast<const u32*>(gain) : nullptr,
+                       (NCTL ? tid - NSW * 64 : tid) * 2, NCTL ? NCTL * 64 : NT, pre);
   prefill();
 
   // 2. Input: wait for the producers, then stage x * g (x times its RMSNorm gain, if any) in
@@ -549,7 +594,9 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
           use(k, bf16lo(w2), bf16hi(w2), gsl ? gsl[k >> 1] : 0u);
         }
       } else {
-        if (!wait_pairs<WBC>(p, st, ract, in_w + (u32)i * in_stride + (u32)k0, kn, gsl, use, ct, nct)) return false;
+        if (!wait_pairs<WBC>(p, st, ract, in_w + (u32)i * in_stride + (u32)k0, kn, gsl, use, ct, nct,
+                             (!MF && s == 0 && i == 0 && early) ? &pre : nullptr))
+          return false;
       }
       if (gain) {
         // Sum of squares so far: one partial per wave and lane in LDS (the stream keeps no
@@ -921,8 +968,14 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
     }
   };
 
-  // 1. Prefetch U units of the own chunk (SP >= U) and claim the second chunk (the ring's
-  //    first round start comes too late in the own chunk), before waiting for the input.
+  // 1. The first batch of input polls (before the prefetch: loads return in issue order),
+  //    then U units of the own chunk (SP >= U), then the claim of the second chunk (the
+  //    ring's first round start comes too late in the own chunk).
+  const __amdgpu_buffer_rsrc_t ract = rsrc(p.act, p.act_bytes);
+  const u32* gsl = o.gain ? reinterpret_cast<const u32*>(o.gain) : nullptr;
+  PairBatch<WBF> pre;
+  const bool early = !o.from_embed && p.b > 0 && K <= NT * 2 * WBF;
+  if (early) issue_pairs<WBF>(ract, o.in_w, K, gsl, tid * 2, NT, pre);
   u32x4 ring[U];
 #pragma unroll
   for (int sl = 0; sl < U; ++sl) issue(ring[sl]);
@@ -933,7 +986,6 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
   }
 
   // 2. Stage the input times its gain (sum of squares on the side).
-  const __amdgpu_buffer_rsrc_t ract = rsrc(p.act, p.act_bytes);
   bool ok = true;
   float rs[B];
 #pragma unroll
@@ -941,7 +993,6 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
     rs[i] = 1.0f;
     for (int k = (i >= p.b ? 0 : K) + tid; k < Kpad; k += NT) xs[i * Kpad + k] = 0.f;
   }
-  const u32* gsl = o.gain ? reinterpret_cast<const u32*>(o.gain) : nullptr;
 #pragma unroll
   for (int i = 0; i < B; ++i) {
     if (i >= p.b || !ok) continue;
@@ -958,7 +1009,8 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
         const u32 w2 = *reinterpret_cast<const u32*>(e + k);
         use(k, bf16lo(w2), bf16hi(w2), gsl ? gsl[k >> 1] : 0u);
       }
-    } else if (!wait_pairs<WBC>(p, st, ract, o.in_w + (u32)i * o.in_stride, K, gsl, use, tid, NT)) {
+    } else if (!wait_pairs<WBC>(p, st, ract, o.in_w + (u32)i * o.in_stride, K, gsl, use, tid, NT,
+                                (i == 0 && early) ? &pre : nullptr)) {
       ok = false;
     }
     if (o.gain) {
