@@ -1176,9 +1176,14 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
 // maximum shared by the wave, then exponentials and weighted V sums. It yields one partial
 // (max, sum, weighted V) per head. Lanes: LPS = d/8 lanes per slot, 8 dims (16 B of K and
 // of V) per lane, so a wave covers 64/LPS slots per pass and the K/V loads are contiguous.
-// The last chunk's item is the group's merger: the others publish their partials as tagged
-// words, and the merger combines them with its own in chunk order (log-sum-exp) and writes
-// the group's attention output.
+// The group's heads are merged by its last M = min(G, nc, workgroups) chunk items: the item
+// of chunk c = nc - 1 - r merges heads r, r + M, r + 2M, ... Every item publishes its partials
+// of the heads it does not merge as tagged words; a merger combines the other chunks' partials
+// of its heads with its own in chunk order (log-sum-exp), so the result does not depend on M,
+// and writes those heads' attention output. A merger waits for items at most M - 1 indices
+// after its own, and an item can only be held up by items at least one queue length (the
+// workgroup count) before it in its workgroup's queue, so with M at most the workgroup count
+// no chain of waits can close on itself.
 
 // Chunk length of this step (see above); spp is the pass width.
 // gran (<= spp) is the work granularity of one wave: chunks shorter than half a pass are
@@ -1210,6 +1215,15 @@ __device__ __forceinline__ bool item_map(CParams& p, const Step& st, int j, int 
     idx -= per;
   }
   return false;
+}
+
+// Makes the eight values computed before any later memory access: a ring slot's data are
+// converted before its refill is issued, so the refill can reuse the slot's registers (a
+// refill hoisted above the conversion would need fresh ones, and copies back, each waiting
+// for its load, at the end of every loop iteration).
+__device__ __forceinline__ void order_before_load(float (&x)[8]) {
+  asm volatile("" : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(x[4]), "+v"(x[5]), "+v"(x[6]), "+v"(x[7])
+               :: "memory");
 }
 
 // Sum within each 8-lane half-row; every lane of it gets the total (DPP).
@@ -1274,39 +1288,44 @@ __device__ __forceinline__ void sum_slot_groups(float (&ls)[GT], float (&acc)[GT
   }
 }
 
-// The merger of (lane i, KV head g): waits for the tagged partials of chunks 0..nc-2 of each
-// of the group's heads (staged into cp next to its own chunk nc-1, already in LDS), combines
-// them in chunk order (log-sum-exp) and writes the attention output of the G query heads.
+// A merger of (lane i, KV head g): chunk c = nc - 1 - r of the group, merging heads r, r + M,
+// ... below G. Waits for the tagged partials of the other chunks of those heads (staged into cp
+// around its own chunk c, already in LDS), combines them in chunk order (log-sum-exp) and
+// writes those heads' attention output.
 template <int D, int GT>
-__device__ __forceinline__ bool merge_group(CParams& p, const Step& st, int l, int i, int g, int nc, float* cp,
-                                            int tid) {
+__device__ __forceinline__ bool merge_group(CParams& p, const Step& st, int l, int i, int g, int c, int nc, int M,
+                                            float* cp, int tid) {
   const int G = p.G, nh = p.nh, row = D + 2;
+  const int r = nc - 1 - c;
+  const int nH = (G - r + M - 1) / M;     // heads merged here
   const __amdgpu_buffer_rsrc_t rpart = rsrc(p.part, (u32)((size_t)p.L * p.b * nh * p.maxc * row * 8));
   const int per_head = nc * row;
   const int others = (nc - 1) * row;      // even: row is even
+  const int below = c * row;              // words of the chunks before this item's own
   // The group's heads are contiguous: [G][maxc][row] words, the first nc chunks in use.
   const u32 w0 = (u32)((((size_t)l * p.b + i) * nh + (size_t)g * G) * p.maxc * row);
   const u32 hstride = (u32)(p.maxc * row);
   auto where = [&](int k, u32& w, float*& d) {
-    const int h = k / others, r = k - h * others;
-    w = w0 + (u32)h * hstride + (u32)r;
-    d = cp + h * per_head + r;
+    const int hi = k / others, rr = k - hi * others;
+    const int o = rr < below ? rr : rr + row;   // skip chunk c (pairs never straddle a row)
+    w = w0 + (u32)(r + hi * M) * hstride + (u32)o;
+    d = cp + hi * per_head + o;
   };
-  const bool ok = wait_copy_map<WB>(p, st, rpart, G * others, where, tid);
+  const bool ok = wait_copy_map<WB>(p, st, rpart, nH * others, where, tid);
   if (__syncthreads_or(!ok)) return false;
   const u32 obase = p.off_o + (u32)l * p.st_o + (u32)i * (u32)(nh * D);
-  for (int u = tid; u < G * D; u += NT) {
-    const int h = u / D, e = u % D;
-    const float* src = cp + h * per_head;
+  for (int u = tid; u < nH * D; u += NT) {
+    const int hi = u / D, e = u % D, h = r + hi * M;
+    const float* src = cp + hi * per_head;
     // The chunks in batches of 8: a batch's reads are issued together (indices past the last
     // chunk read the last chunk again and are dropped by a select), then used in chunk order.
-    float M = -INFINITY, den = 0.f, num = 0.f;
+    float mx = -INFINITY, den = 0.f, num = 0.f;
     for (int c0 = 0; c0 < nc; c0 += 8) {
       float mv[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) mv[k] = src[min(c0 + k, nc - 1) * row + D];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) M = fmaxf(M, c0 + k < nc ? mv[k] : -INFINITY);
+      for (int k = 0; k < 8; ++k) mx = fmaxf(mx, c0 + k < nc ? mv[k] : -INFINITY);
     }
     for (int c0 = 0; c0 < nc; c0 += 8) {
       float mv[8], lv[8], ov[8];
@@ -1319,7 +1338,7 @@ __device__ __forceinline__ bool merge_group(CParams& p, const Step& st, int l, i
       }
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const float f = c0 + k < nc ? exp2f(mv[k] - M) : 0.f;
+        const float f = c0 + k < nc ? exp2f(mv[k] - mx) : 0.f;
         den += f * lv[k];
         num += f * ov[k];
       }
@@ -1350,7 +1369,7 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
   i = uni(i); g = uni(g); c = uni(c); nc = uni(nc); t0 = uni(t0); t1 = uni(t1);
   const int G = p.G;
   const int kvl = uni(st.kvl[i]);
-  const bool is_last = (t1 == kvl + 1);     // holds the new slot; merges the group
+  const bool is_last = (t1 == kvl + 1);     // holds the new slot
   const int t_end = min(t1, kvl);            // slots [t0, t_end) come from the arena
   const int ssl = lane / LPS, de = (lane % LPS) * 8;
   CLayerPtrs& Lw = ((CLayerPtrs*)p.layers)[l];
@@ -1639,7 +1658,10 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
     // and the weighted V sums. Because the maximum is the same in every lane, the wave's slot
     // groups are combined at the end by plain sums, with no rescaling. ok[s] says the wave holds
     // pass s; val[s] that this lane's slot in it is live. refill_k / refill_v(s) are called once
-    // pass s's K (V) registers are no longer needed.
+    // pass s's K (V) registers are no longer needed, for every s: loads under a branch would
+    // leave the compiler unsure how many loads follow each slot's, and it would then wait for
+    // all of them (the refill just issued included) before every slot. Passes past the chunk
+    // load zeros.
     auto block = [&](auto nbc, const u32x4* kw, const u32x4* vw, const bool* ok, const bool* val, auto refill_k,
                      auto refill_v) {
       constexpr int NB = decltype(nbc)::value;
@@ -1648,11 +1670,12 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
       for (int s = 0; s < NB; ++s) {
   #pragma unroll
         for (int h = 0; h < GT; ++h) sc[s][h] = -INFINITY;
+        const u32x4 k = kw[s];
+        float kf[8] = {bf16lo(k.x), bf16hi(k.x), bf16lo(k.y), bf16hi(k.y),
+                       bf16lo(k.z), bf16hi(k.z), bf16lo(k.w), bf16hi(k.w)};
+        order_before_load(kf);
+        refill_k(s);
         if (ok[s]) {
-          const u32x4 k = kw[s];
-          const float kf[8] = {bf16lo(k.x), bf16hi(k.x), bf16lo(k.y), bf16hi(k.y),
-                               bf16lo(k.z), bf16hi(k.z), bf16lo(k.w), bf16hi(k.w)};
-          refill_k(s);
   #pragma unroll
           for (int h = 0; h < GT; ++h) {
             if (h < G) {
@@ -1680,11 +1703,12 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
       }
   #pragma unroll
       for (int s = 0; s < NB; ++s) {
+        const u32x4 v = vw[s];
+        float vf[8] = {bf16lo(v.x), bf16hi(v.x), bf16lo(v.y), bf16hi(v.y),
+                       bf16lo(v.z), bf16hi(v.z), bf16lo(v.w), bf16hi(v.w)};
+        order_before_load(vf);
+        refill_v(s);
         if (ok[s]) {
-          const u32x4 v = vw[s];
-          const float vf[8] = {bf16lo(v.x), bf16hi(v.x), bf16lo(v.y), bf16hi(v.y),
-                               bf16lo(v.z), bf16hi(v.z), bf16lo(v.w), bf16hi(v.w)};
-          refill_v(s);
   #pragma unroll
           for (int h = 0; h < GT; ++h) {
             const float pw = (sc[s][h] == -INFINITY) ? 0.f : exp2f(sc[s][h] - m[h]);
@@ -1698,16 +1722,28 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
     if (tl && tid == 0) tl[2] = clock_now();
     const int n_arena = t_end - t0;
     const int npass = n_arena > 0 ? (n_arena + SPP - 1) / SPP : 0;
-    for (int pb = 0; pb < npass; pb += NPF) {
+    // Full blocks with more passes after them refill the ring in place (every pass held, no
+    // branch); the last block, full or not, only consumes. Within a block the compiler then
+    // waits for each slot's own loads only.
+    int pb = 0;
+    for (; pb + NPF < npass; pb += NPF) {
       bool ok[NPF], val[NPF];
   #pragma unroll
       for (int sl = 0; sl < NPF; ++sl) {
-        const int pass = pb + sl;
-        ok[sl] = pass < npass;
-        val[sl] = t0 + pass * SPP + wave * SPW + ssl < t_end;
+        ok[sl] = true;
+        val[sl] = t0 + (pb + sl) * SPP + wave * SPW + ssl < t_end;
       }
       block(std::integral_constant<int, NPF>{}, kr, vr, ok, val,
             [&](int sl) { issue_k(sl, pb + sl + NPF); }, [&](int sl) { issue_v(sl, pb + sl + NPF); });
+    }
+    if (pb < npass) {
+      bool ok[NPF], val[NPF];
+  #pragma unroll
+      for (int sl = 0; sl < NPF; ++sl) {
+        ok[sl] = pb + sl < npass;
+        val[sl] = t0 + (pb + sl) * SPP + wave * SPW + ssl < t_end;
+      }
+      block(std::integral_constant<int, NPF>{}, kr, vr, ok, val, [](int) {}, [](int) {});
     }
     if (is_last && wave == 0) {
       // The new slot, as stored (bf16), in the first slot group of wave 0.
@@ -1739,10 +1775,12 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
   }
   __syncthreads();
   if (tl && tid == 0) tl[7] = clock_now();
-  // Merge the waves in order: the chunk's partial for each head. The merger keeps its own in
-  // LDS (slot nc - 1 of cp); the other items publish theirs as tagged words.
+  // Merge the waves in order: the chunk's partial for each head. A merger keeps its own of the
+  // heads it merges in LDS (slot c of cp); the rest are published as tagged words.
   const int nh = p.nh;
   const int row = D + 2;
+  const int NM = uni(min(min(G, nc), (int)p.nwg));  // mergers of the group (see above)
+  const int mr = nc - 1 - c;                         // merger rank, when below NM
   for (int u = tid; u < G * row; u += NT) {
     const int h = u / row, e = u % row;
     // Every wave's maximum and value first (all reads in flight together), then the sum in
@@ -1763,15 +1801,15 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
       A += vw[w] * (mw[w] == -INFINITY ? 0.f : f);   // e == D + 1 sums the softmax denominators
     }
     const float val = (e == D) ? M : A;
-    if (is_last) {
-      cp[(h * nc + (nc - 1)) * row + e] = val;
+    if (mr < NM && h % NM == mr) {
+      cp[((h / NM) * nc + c) * row + e] = val;
     } else {
       u64* dst = p.part + ((((size_t)l * p.b + i) * nh + g * G + h) * p.maxc + c) * row;
       st_tag(dst + e, val, st.epoch);
     }
   }
   if (tl && tid == 0) tl[3] = clock_now();
-  if (is_last && !merge_group<D, GT>(p, st, l, i, g, nc, cp, tid)) return false;
+  if (mr < NM && !merge_group<D, GT>(p, st, l, i, g, c, nc, NM, cp, tid)) return false;
   __syncthreads();   // LDS is reused by the next instruction
   return true;
 }
