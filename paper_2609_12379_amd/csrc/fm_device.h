@@ -150,12 +150,22 @@ __device__ __forceinline__ void st_tag(u64* p, float v, u32 epoch) {
   __hip_atomic_store(p, tag(v, epoch), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Value of another lane of the same 16-lane row (DPP control ctl: a lane permutation inside
+// each quad, a mirror or a rotation of the row, for which every lane has a source). Written as
+// a DPP update with bound_ctrl so that an add of the result folds into one v_add_f32_dpp.
+template <int CTL>
+__device__ __forceinline__ float dpp_row(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTL, 0xF, 0xF, true));
+}
+constexpr int DPP_QUAD_1032 = 0xB1, DPP_QUAD_2301 = 0x4E, DPP_HALF_MIRROR = 0x141, DPP_MIRROR = 0x140;
+constexpr int DPP_ROR4 = 0x124, DPP_ROR8 = 0x128;
+
 // Sum within each 16-lane row; every lane of the row gets the total (DPP, no LDS).
 __device__ __forceinline__ float row16_sum(float s) {
-  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0xB1, 0xF, 0xF, false));   // quad [1,0,3,2]
-  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x4E, 0xF, 0xF, false));   // quad [2,3,0,1]
-  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x141, 0xF, 0xF, false));  // half-row mirror
-  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x140, 0xF, 0xF, false));  // row mirror
+  s += dpp_row<DPP_QUAD_1032>(s);
+  s += dpp_row<DPP_QUAD_2301>(s);
+  s += dpp_row<DPP_HALF_MIRROR>(s);
+  s += dpp_row<DPP_MIRROR>(s);
   return s;
 }
 

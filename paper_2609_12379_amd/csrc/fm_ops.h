@@ -1228,9 +1228,9 @@ __device__ __forceinline__ void order_before_load(float (&x)[8]) {
 
 // Sum within each 8-lane half-row; every lane of it gets the total (DPP).
 __device__ __forceinline__ float row8_sum(float s) {
-  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0xB1, 0xF, 0xF, false));   // quad [1,0,3,2]
-  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x4E, 0xF, 0xF, false));   // quad [2,3,0,1]
-  s += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s), 0x141, 0xF, 0xF, false));  // half-row mirror
+  s += dpp_row<DPP_QUAD_1032>(s);
+  s += dpp_row<DPP_QUAD_2301>(s);
+  s += dpp_row<DPP_HALF_MIRROR>(s);
   return s;
 }
 
@@ -1646,10 +1646,13 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
   #pragma unroll
       for (int e = 0; e < 8; ++e) qr[h][e] = (h < G) ? v[e] * p.q_scale : 0.f;
     }
+    // The running maxima start at -FLT_MAX rather than -inf, so that every exponent below is
+    // m - m' or s - m with m finite: never inf - inf, and exp2 of -inf (an empty slot) is 0.
+    // That lets the hardware exp2 run unguarded; its arguments are never positive.
     float m[GT], ls[GT], acc[GT][8];
   #pragma unroll
     for (int h = 0; h < GT; ++h) {
-      m[h] = -INFINITY; ls[h] = 0.f;
+      m[h] = -3.40282347e38f; ls[h] = 0.f;   // -FLT_MAX
   #pragma unroll
       for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
     }
@@ -1695,7 +1698,7 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
         for (int s = 1; s < NB; ++s) bm = fmaxf(bm, sc[s][h]);
         bm = max_slot_groups<LPS>(bm, lane);
         const float mn = fmaxf(m[h], bm);
-        const float a = (m[h] == -INFINITY) ? 0.f : exp2f(m[h] - mn);
+        const float a = __builtin_amdgcn_exp2f(m[h] - mn);
         ls[h] *= a;
   #pragma unroll
         for (int e = 0; e < 8; ++e) acc[h][e] *= a;
@@ -1711,7 +1714,7 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
         if (ok[s]) {
   #pragma unroll
           for (int h = 0; h < GT; ++h) {
-            const float pw = (sc[s][h] == -INFINITY) ? 0.f : exp2f(sc[s][h] - m[h]);
+            const float pw = __builtin_amdgcn_exp2f(sc[s][h] - m[h]);
             ls[h] += pw;
   #pragma unroll
             for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pw, vf[e], acc[h][e]);
