@@ -126,6 +126,10 @@ __device__ __forceinline__ bool finish_pairs(CParams& p, const Step& st, __amdgp
 // inputs are polled after the prefetch in full batches as before (split, they would cost an
 // extra round trip).
 constexpr int WBF = 4;
+// Pairs per thread in one batch for long inputs of the batch-1 dynamic-chunk stages (up to
+// 14336 values: the down projection's input on the 7B-13B shapes), which would otherwise take
+// two round trips. (At batch 2 the registers are not there.)
+constexpr int WBL = 14;
 
 // first: the caller's first WBF pairs (k0 = t * 2), already issued with the same arguments, or
 // null.
@@ -1009,6 +1013,9 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
         const u32 w2 = *reinterpret_cast<const u32*>(e + k);
         use(k, bf16lo(w2), bf16hi(w2), gsl ? gsl[k >> 1] : 0u);
       }
+    } else if (B == 1 && K > NT * 2 * WBC && K <= NT * 2 * WBL) {
+      if constexpr (B == 1)
+        if (!wait_pairs<WBL>(p, st, ract, o.in_w + (u32)i * o.in_stride, K, gsl, use, tid, NT)) ok = false;
     } else if (!wait_pairs<WBC>(p, st, ract, o.in_w + (u32)i * o.in_stride, K, gsl, use, tid, NT,
                                 (i == 0 && early) ? &pre : nullptr)) {
       ok = false;
