@@ -48,6 +48,12 @@ constexpr int NSW = NWAVE - NCTL;
 // Matrix-core (batched) tiles need fewer row sums and a larger slab.
 constexpr int LDS_FLOATS = 40448;
 constexpr int MISC_FLOATS = 1024;   // block reductions, argmax keys, chunk ids; timeline marks in the last 24
+// Each lane's token, position and KV length for the step, copied into the misc area at
+// kernel start (words LANE_IN .. LANE_IN + 24: tokens, then positions, then KV lengths, 8
+// each). Read through an LDS pointer they wait on no memory counter, so reading them never
+// waits for loads or stores in flight.
+constexpr int LANE_IN = 640;
+typedef __attribute__((address_space(3))) int lds_i32;
 constexpr int RESID_FLOATS = 2048;  // residual rows staged for the epilogue
 constexpr int ATT_FLOATS = 9600;    // q heads, k, v and per-wave partials of one item (G <= 8, d <= 128)
 template <int B> constexpr int rowacc_floats() { return B >= 4 ? 4096 : 8192; }
@@ -216,6 +222,9 @@ __device__ __forceinline__ u64 clock_now() { return wall_clock64(); }
 // when it ends): a store to memory in the middle of an operator would make its next full wait
 // for loads also wait for the store's acknowledgement.
 typedef __attribute__((address_space(3))) u64 tl_t;
+__device__ __forceinline__ lds_i32* lane_inputs(float* smem) {
+  return (lds_i32*)(__attribute__((address_space(3))) float*)(smem + LDS_FLOATS - MISC_FLOATS + LANE_IN);
+}
 
 // Watchdog bound on any single wait (wall clock runs at 100 MHz on MI355X): 2 s.
 constexpr u64 WAIT_TICKS = 200000000ull;

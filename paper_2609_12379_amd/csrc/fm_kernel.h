@@ -22,6 +22,10 @@ __global__ __launch_bounds__(NT, 1) void step_kernel(const Params* __restrict__ 
   u32 code = 0;
   if (tid < p.b) {
     const int t = st.tok[tid], ps = st.pos[tid], kl = st.kvl[tid];
+    lds_i32* lin = lane_inputs(smem);
+    lin[tid] = t;
+    lin[8 + tid] = ps;
+    lin[16 + tid] = kl;
     if (t < 0 || t >= p.V) code = FM_DEV_BAD_TOKEN;
     else if (ps < 0 || ps >= p.max_ctx) code = FM_DEV_BAD_POSITION;
     else if (kl < 0 || kl >= p.max_ctx) code = FM_DEV_BAD_KV_LEN;

@@ -205,17 +205,50 @@ __device__ __forceinline__ bool wait_copy_map(CParams& p, const Step& st, __amdg
   return true;
 }
 
-// Like wait_copy for three word ranges at once (one round trip when all are ready).
-__device__ __forceinline__ bool wait_copy3(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra,
-                                           u32 wa, int na, float* da, u32 wb, int nb, float* db,
-                                           u32 wc, int nc, float* dc, int tid) {
-  auto where = [&](int k, u32& w, float*& d) {
-    if (k < na) { w = wa + (u32)k; d = da + k; }
-    else if (k < na + nb) { w = wb + (u32)(k - na); d = db + (k - na); }
-    else { w = wc + (u32)(k - na - nb); d = dc + (k - na - nb); }
-  };
-  return wait_copy_map<WB>(p, st, ra, na + nb + nc, where, tid);
+// wait_copy_map in two halves for inputs of at most NT * 2 * WBT words (one batch): the
+// polls are issued first, other loads may follow, and the caller finishes later; loads
+// return in issue order, so the polls are not held up by what was issued after them.
+template <int WBT>
+struct MapBatch {
+  u32x4 v[WBT];
+  u32 w[WBT];
+};
+
+template <int WBT, class Where>
+__device__ __forceinline__ void issue_map(__amdgpu_buffer_rsrc_t ra, int n, Where where, int tid, MapBatch<WBT>& b) {
+#pragma unroll
+  for (int j = 0; j < WBT; ++j) {
+    const int k = tid * 2 + j * NT * 2;
+    float* d = nullptr;
+    b.w[j] = 0x1FFFFFFEu;
+    if (k < n) where(k, b.w[j], d);
+    b.v[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, (k < n) ? b.w[j] * 8u : 0xFFFFFFF0u, 0, CPOL_SC1);
+  }
 }
+
+template <int WBT, class Where>
+__device__ __forceinline__ bool finish_map(CParams& p, const Step& st, __amdgpu_buffer_rsrc_t ra, int n, Where where,
+                                           int tid, MapBatch<WBT>& b) {
+  u32 pend = 0;
+#pragma unroll
+  for (int j = 0; j < WBT; ++j) {
+    const int k = tid * 2 + j * NT * 2;
+    if (k < n && (b.v[j].y != st.epoch || b.v[j].w != st.epoch)) pend |= 1u << j;
+  }
+  if (pend && !repoll<WBT>(p, st, ra, b.w, b.v, pend)) return false;
+#pragma unroll
+  for (int j = 0; j < WBT; ++j) {
+    const int k = tid * 2 + j * NT * 2;
+    if (k < n) {
+      u32 ww; float* d;
+      where(k, ww, d);
+      d[0] = __uint_as_float(b.v[j].x);
+      d[1] = __uint_as_float(b.v[j].z);
+    }
+  }
+  return true;
+}
+
 
 // Sum over the workgroup; every thread gets the total. Uses misc[0..NWAVE).
 __device__ __forceinline__ float block_sum(float v, float* misc, int lane, int wave) {
@@ -507,6 +540,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
   float* rowacc = smem + XSF;            // [KP][nr][NW][B]
   float* resid = rowacc + rowacc_floats<B>();
   float* misc = smem + LDS_FLOATS - MISC_FLOATS;
+  const lds_i32* lin = lane_inputs(smem);            // this step's tokens at lin[0 .. b)
 
   // 1. Prefetch this wave's first U units, before waiting for the input.
   const uint16_t* zp = zero_slot(p, wave, lane);
@@ -592,7 +626,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
         put_pair(i, k, a, b);
       };
       if (from_embed) {
-        const uint16_t* e = p.embed + (size_t)st.tok[i] * p.h + k0;
+        const uint16_t* e = p.embed + (size_t)lin[i] * p.h + k0;
         for (int k = ct * 2; k < kn; k += nct * 2) {
           const u32 w2 = *reinterpret_cast<const u32*>(e + k);
           use(k, bf16lo(w2), bf16hi(w2), gsl ? gsl[k >> 1] : 0u);
@@ -618,7 +652,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
     for (int i = 0; i < B && ok; ++i) {
       if (i >= p.b) continue;
       if (res_embed) {
-        const uint16_t* e = p.embed + (size_t)st.tok[i] * p.h;
+        const uint16_t* e = p.embed + (size_t)lin[i] * p.h;
         for (int k = ct; k < nr; k += nct) resid[i * nr + k] = __uint_as_float((u32)e[ra + k] << 16);
       } else {
         const int lo = ra & ~1, hi = (rb + 1) & ~1;
@@ -756,7 +790,7 @@ __device__ __forceinline__ bool op_gemv(CParams& p, const Step& st, const int32_
                        : st.taps + ((size_t)l * p.b + i) * p.tap_block + off;
         for (int k = tid; k < K; k += NT) {
           const float x = from_embed
-              ? __uint_as_float((u32)p.embed[(size_t)st.tok[i] * p.h + k] << 16)
+              ? __uint_as_float((u32)p.embed[(size_t)lin[i] * p.h + k] << 16)
               : __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ract, (in_w + (u32)i * in_stride + (u32)k) * 8u,
                                                                       0, CPOL_SC1));
           t[k] = x * rs[i] * __uint_as_float((u32)gain[k] << 16);
@@ -875,6 +909,7 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
   float* rowacc = smem + xslab_floats<B>();          // [nslot][KP][nwr][B] row part sums
   float* misc = smem + LDS_FLOATS - MISC_FLOATS;
   float* mss = misc + 512;                           // [NWAVE][B] partial sums of squares
+  const lds_i32* lin = lane_inputs(smem);            // this step's tokens at lin[0 .. b)
   lds_int* chl = (lds_int*)(__attribute__((address_space(3))) int*)(misc + 256);   // [nslot + 1] chunk ids
 
   // The schedule guarantees these; a violation would overrun LDS, so it stops the step.
@@ -1008,7 +1043,7 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
       xs[i * Kpad + k + 1] = b;
     };
     if (o.from_embed) {
-      const uint16_t* e = p.embed + (size_t)st.tok[i] * p.h;
+      const uint16_t* e = p.embed + (size_t)lin[i] * p.h;
       for (int k = tid * 2; k < K; k += NT * 2) {
         const u32 w2 = *reinterpret_cast<const u32*>(e + k);
         use(k, bf16lo(w2), bf16hi(w2), gsl ? gsl[k >> 1] : 0u);
@@ -1108,7 +1143,7 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
                        : st.taps + ((size_t)l * p.b + i) * p.tap_block + off;
         for (int k = tid; k < K; k += NT) {
           const float x = o.from_embed
-              ? __uint_as_float((u32)p.embed[(size_t)st.tok[i] * p.h + k] << 16)
+              ? __uint_as_float((u32)p.embed[(size_t)lin[i] * p.h + k] << 16)
               : __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ract, (o.in_w + (u32)i * o.in_stride + (u32)k) * 8u,
                                                                       0, CPOL_SC1));
           t[k] = x * rs[i] * __uint_as_float((u32)o.gain[k] << 16);
@@ -1135,7 +1170,7 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
       float res = 0.f;
       if (o.has_res) {
         if (o.res_embed) {
-          res = __uint_as_float((u32)p.embed[(size_t)st.tok[i] * p.h + r] << 16);
+          res = __uint_as_float((u32)p.embed[(size_t)lin[i] * p.h + r] << 16);
         } else {
           float ra_, rb_;
           if (!wait_pair(p, st, ract, o.res_w + (u32)i * o.res_stride + (u32)(r & ~1), ra_, rb_)) { ok = false; break; }
@@ -1196,9 +1231,9 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
 // gran (<= spp) is the work granularity of one wave: chunks shorter than half a pass are
 // rounded to it instead (short contexts then keep many items, each on a few waves). tmin is
 // the shortest chunk worth its share of the merge.
-__device__ __forceinline__ int chunk_len(CParams& p, const Step& st, int spp, int gran, int tmin) {
+__device__ __forceinline__ int chunk_len(CParams& p, const lds_i32* kvls, int spp, int gran, int tmin) {
   long long total = 0;
-  for (int ii = 0; ii < p.b; ++ii) total += st.kvl[ii] + 1;
+  for (int ii = 0; ii < p.b; ++ii) total += kvls[ii] + 1;
   total *= p.nkv;
   const long long denom = p.P - p.nkv * p.b;
   const int T0 = (int)((total + denom - 1) / denom);
@@ -1206,12 +1241,12 @@ __device__ __forceinline__ int chunk_len(CParams& p, const Step& st, int spp, in
   return max(((T0 + q - 1) / q) * q, tmin);
 }
 
-__device__ __forceinline__ bool item_map(CParams& p, const Step& st, int j, int spp, int gran, int tmin, int& i,
+__device__ __forceinline__ bool item_map(CParams& p, const lds_i32* kvls, int j, int spp, int gran, int tmin, int& i,
                                          int& g, int& c, int& nc, int& t0, int& t1) {
-  const int T = chunk_len(p, st, spp, gran, tmin);
+  const int T = chunk_len(p, kvls, spp, gran, tmin);
   int idx = j;
   for (int ii = 0; ii < p.b; ++ii) {
-    const int W = st.kvl[ii] + 1;
+    const int W = kvls[ii] + 1;
     const int n = (W + T - 1) / T;
     const int per = p.nkv * n;
     if (idx < per) {
@@ -1372,10 +1407,11 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
   int i, g, c, nc, t0, t1;
   // VALU items cover at least 64 slots (two passes at d = 128): shorter chunks cost the merger
   // more than they save (measured on the Qwen3-0.6B shape at context 512).
-  if (!item_map(p, st, j, SPP, MFA ? 16 : SPP, MFA ? 16 : 64, i, g, c, nc, t0, t1)) return true;
+  const lds_i32* lin = lane_inputs(smem);
+  if (!item_map(p, lin + 16, j, SPP, MFA ? 16 : SPP, MFA ? 16 : 64, i, g, c, nc, t0, t1)) return true;
   i = uni(i); g = uni(g); c = uni(c); nc = uni(nc); t0 = uni(t0); t1 = uni(t1);
   const int G = p.G;
-  const int kvl = uni(st.kvl[i]);
+  const int kvl = uni(lin[16 + i]);
   const bool is_last = (t1 == kvl + 1);     // holds the new slot
   const int t_end = min(t1, kvl);            // slots [t0, t_end) come from the arena
   const int ssl = lane / LPS, de = (lane % LPS) * 8;
@@ -1384,6 +1420,43 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
   const __amdgpu_buffer_rsrc_t rk = rsrc(Lw.kc, arena_bytes);
   const __amdgpu_buffer_rsrc_t rv = rsrc(Lw.vc, arena_bytes);
   const u32 head_slot0 = ((u32)i * p.nkv + (u32)g) * (u32)p.max_ctx;
+
+  // This lane's rotary row and the QK-norm gains (they depend on no activation of this step),
+  // then the q/k/v polls, then the K/V prefetch.
+  const int half = D / 2;
+  const float* rt = p.rope + (size_t)lin[8 + i] * half * 2;
+  float2 rot = make_float2(1.f, 0.f);
+  const int pe = tid % half;                  // rotary pair this thread applies
+  rot = *reinterpret_cast<const float2*>(rt + pe * 2);
+  // QK-norm gains (bf16) for dims lane and lane + 64, converted only once the polls are
+  // checked (bf16 1.0 without QK-norm).
+  u32 gq_b = 0x3F80u, gk_b = 0x3F80u, gq2_b = 0x3F80u, gk2_b = 0x3F80u;
+  if (p.qk_norm) {
+    gq_b = Lw.q_norm[lane];
+    gk_b = Lw.k_norm[lane];
+    if (D > 64) {
+      gq2_b = Lw.q_norm[lane + 64];
+      gk2_b = Lw.k_norm[lane + 64];
+    }
+  }
+
+  // The q/k/v polls go out first (loads return in issue order: a poll behind the prefetch
+  // could not report ready inputs before the prefetch had landed).
+  const __amdgpu_buffer_rsrc_t ract = rsrc(p.act, p.act_bytes);
+  const u32 base = p.off_qkv + (u32)l * p.st_qkv + (u32)i * (u32)((p.nh + 2 * p.nkv) * D);
+  const int n3 = G * D + 2 * D;
+  float* qs = smem + LDS_FLOATS - MISC_FLOATS - ATT_FLOATS;  // [G][D]
+  float* ks = qs + GT * D;          // [D]
+  float* vs = ks + D;               // [D]
+  const u32 wq = base + (u32)(g * G * D), wk = base + (u32)(p.nh * D + g * D), wv = base + (u32)((p.nh + p.nkv) * D + g * D);
+  auto where3 = [&](int k, u32& w, float*& d) {
+    if (k < G * D) { w = wq + (u32)k; d = qs + k; }
+    else if (k < G * D + D) { w = wk + (u32)(k - G * D); d = ks + (k - G * D); }
+    else { w = wv + (u32)(k - G * D - D); d = vs + (k - G * D - D); }
+  };
+  static_assert((GT + 2) * D <= NT * 2 * 2, "q, k and v fit one poll batch of two pairs per thread");
+  MapBatch<2> qkv_polls;
+  issue_map<2>(ract, n3, where3, tid, qkv_polls);
 
   // Prefetch, before waiting for q: the first K/V of this wave (NPF passes, or two tiles),
   // this lane's rotary row and the QK-norm gains (none of them depend on this step's
@@ -1417,37 +1490,23 @@ __device__ __forceinline__ bool op_attn(CParams& p, const Step& st, const int32_
 #pragma unroll
     for (int s = 0; s < NPF; ++s) { issue_k(s, s); issue_v(s, s); }
   }
-  const int half = D / 2;
-  const float* rt = p.rope + (size_t)st.pos[i] * half * 2;
-  float2 rot = make_float2(1.f, 0.f);
-  const int pe = tid % half;                  // rotary pair this thread applies
-  rot = *reinterpret_cast<const float2*>(rt + pe * 2);
-  float gq = 1.f, gk = 1.f;                   // QK-norm gains for dims lane and lane + 64
-  float gq2 = 1.f, gk2 = 1.f;
-  if (p.qk_norm) {
-    gq = __uint_as_float((u32)Lw.q_norm[lane] << 16);
-    gk = __uint_as_float((u32)Lw.k_norm[lane] << 16);
-    if (D > 64) {
-      gq2 = __uint_as_float((u32)Lw.q_norm[lane + 64] << 16);
-      gk2 = __uint_as_float((u32)Lw.k_norm[lane + 64] << 16);
-    }
-  }
-
   // LDS: the merger's partials at the start, this item's working vectors near the end.
   static_assert(GT * D + 2 * D + NWAVE * GT * (D + 2) <= ATT_FLOATS, "attention LDS");
   static_assert(kMergeFloats + 3 * KB * 64 * 4 <= LDS_FLOATS - MISC_FLOATS - ATT_FLOATS, "q planes in LDS");
   static_assert(NWAVE * 16 * VROW <= 2 * kMergeFloats, "V tiles in the merge region");
   float* cp = smem;                 // [G][nc][D + 2], at most kMergeFloats
-  float* qs = smem + LDS_FLOATS - MISC_FLOATS - ATT_FLOATS;  // [G][D]
-  float* ks = qs + GT * D;          // [D]
-  float* vs = ks + D;               // [D]
   float* wst = vs + D;              // [NWAVE][GT][D + 2]
 
-  // Wait for this group's q heads, k and v (one batched round trip).
-  const __amdgpu_buffer_rsrc_t ract = rsrc(p.act, p.act_bytes);
-  const u32 base = p.off_qkv + (u32)l * p.st_qkv + (u32)i * (u32)((p.nh + 2 * p.nkv) * D);
-  bool ok = wait_copy3(p, st, ract, base + (u32)(g * G * D), G * D, qs, base + (u32)(p.nh * D + g * D), D, ks,
-                       base + (u32)((p.nh + p.nkv) * D + g * D), D, vs, tid);
+  // The first uses of the polls, the rotary row and the gains stay behind the prefetch: the
+  // compiler would otherwise wait for them between the prefetch's loads (and a wait for any
+  // load also waits for the previous instruction's stores).
+  asm volatile("" : "+v"(qkv_polls.v[0]), "+v"(qkv_polls.v[1]), "+v"(rot), "+v"(gq_b), "+v"(gk_b), "+v"(gq2_b),
+               "+v"(gk2_b) :: "memory");
+  const float gq = __uint_as_float(gq_b << 16), gk = __uint_as_float(gk_b << 16);
+  const float gq2 = __uint_as_float(gq2_b << 16), gk2 = __uint_as_float(gk2_b << 16);
+
+  // Wait for this group's q heads, k and v (one batched round trip when they are ready).
+  bool ok = finish_map<2>(p, st, ract, n3, where3, tid, qkv_polls);
   if (__syncthreads_or(!ok)) return false;
   if (tl && tid == 0) tl[1] = clock_now();
 
