@@ -36,13 +36,25 @@ __global__ __launch_bounds__(NT, 1) void step_kernel(const Params* __restrict__ 
   }
   if (abort_raised(p)) return;
 
+  // Queue bounds and instruction words come in by scalar loads (constant address space, counted
+  // by lgkmcnt): a vector load would be waited for with vmcnt, which first waits for every
+  // store of the previous instruction to be acknowledged. The tables are written by the host
+  // before the launch and never during it. (At batch 4 and 8 it measured slower: the wider
+  // tiles need those scalar registers, and the matrix-core tiles would spill.)
+  typedef const __attribute__((address_space(4))) int32_t cq_t;
+  constexpr bool SCAL = B <= 2;
   int q0, q1;
   if (st.stage < 0) {
-    q0 = p.qoff[wg];
-    q1 = p.qoff[wg + 1];
+    q0 = SCAL ? ((const cq_t*)p.qoff)[wg] : p.qoff[wg];
+    q1 = SCAL ? ((const cq_t*)p.qoff)[wg + 1] : p.qoff[wg + 1];
   } else {
-    q0 = p.stage_rng[((size_t)st.stage * p.nwg + wg) * 2];
-    q1 = p.stage_rng[((size_t)st.stage * p.nwg + wg) * 2 + 1];
+    const size_t k = ((size_t)st.stage * p.nwg + wg) * 2;
+    q0 = SCAL ? ((const cq_t*)p.stage_rng)[k] : p.stage_rng[k];
+    q1 = SCAL ? ((const cq_t*)p.stage_rng)[k + 1] : p.stage_rng[k + 1];
+  }
+  if constexpr (SCAL) {
+    q0 = __builtin_amdgcn_readfirstlane(q0);
+    q1 = __builtin_amdgcn_readfirstlane(q1);
   }
   for (int q = q0; q < q1; ++q) {
     // Re-derive the parameter pointer per instruction, opaquely: the compiler then reloads
@@ -51,7 +63,13 @@ __global__ __launch_bounds__(NT, 1) void step_kernel(const Params* __restrict__ 
     CParams* pp = (CParams*)pparams;
     asm volatile("" : "+s"(pp));
     CParams& P = *pp;
-    const int32_t* ins = P.instrs + 4 * (size_t)q;
+    const int32_t* insg = P.instrs + 4 * (size_t)q;
+    int32_t iw[4];
+    if constexpr (SCAL) {
+      const cq_t* insc = (const cq_t*)insg;
+      iw[0] = insc[0]; iw[1] = insc[1]; iw[2] = insc[2]; iw[3] = insc[3];
+    }
+    const int32_t* ins = SCAL ? iw : insg;
     const int op = ins[0];
     u64* tg = st.timeline ? st.timeline + 8 * (size_t)q : nullptr;
     tl_t* tl = tg ? (tl_t*)(__attribute__((address_space(3))) float*)(smem + LDS_FLOATS - 24) : nullptr;   // 8 marks

@@ -1120,6 +1120,10 @@ __device__ __forceinline__ bool op_gemv_dyn(CParams& p, const Step& st, const in
       issue(ring[sl]);
     }
   }
+  // The ring's last refills (zero-page reads) are still in flight: let them land here, before
+  // the epilogue's stores, so that no load is pending on a register the next instruction
+  // writes (the compiler would wait for it there, behind these stores' acknowledgements).
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
   __syncthreads();
   if (tl && tid == 0) tl[3] = clock_now();
   // Every wave walked the same slots: the consume cursor stopped at the first empty one.
