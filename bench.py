@@ -208,7 +208,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=64)
-    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--warmup", type=int, default=64)
     ap.add_argument("--config", default="llama2-7b")
     ap.add_argument("--extra", default="qwen3-8b-b1,llama2-13b-b1",
                     help="other workloads timed in the same run (comma-separated; empty for none)")
