@@ -156,7 +156,7 @@ fm_status fm_decode_step(fm_handle *h, const int32_t *token_ids, const int32_t *
  * attention, O-projection, gate/up and down launch, plus one LM-head launch. Each launch
  * runs the same device code on the same per-CU queues and keeps the fusions inside its
  * stage (RMSNorm in the projection's staging, QK-norm, RoPE and the KV append in the
- * attention items, the split-KV merge in each group's last item). This per-stage ablation
+ * attention items, the split-KV merge in each group's last items). This per-stage ablation
  * measures what the single launch saves in launches and drains between stages (the launch
  * and synchronisation costs of split-step engines, Sec. 1 and Sec. 5.2.3). Arguments and
  * results are as for fm_decode_step. The outputs are bit-identical to it. */
@@ -242,7 +242,8 @@ size_t fm_tap_count(const fm_model_cfg *cfg);
  * non-NULL, each step records per queued instruction q, at buf[8q..8q+7], the device
  * wall-clock ticks {start, inputs ready, prologue done, stream done, end, workgroup, a, b}.
  * For attention items the middle marks are: q/k/v ready, rotary and KV append done, partials
- * published; the span from there to the end is the group merge (last item of a group only);
+ * published; the span from there to the end is the merge of the item's heads (only in a
+ * group's last min(G, chunks, workgroups) items, each merging every such count-th head);
  * a = the item's slot passes done, b = its waves' partials gathered in LDS. GEMV tiles leave
  * a and b 0, except that a GEMV stage in dynamic chunks records in a the number of chunks the
  * workgroup took (a count, not a time).

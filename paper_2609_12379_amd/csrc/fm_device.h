@@ -8,8 +8,8 @@
 //     counter, so a handoff costs one store and one read round trip. There is no separate
 //     flag, no grid barrier, and no L2 writeback or invalidate (both cost microseconds on
 //     MI355X's eight non-coherent XCD L2s).
-//   * Attention partials are tagged words too. The item holding a (lane, KV head) group's
-//     last chunk waits for the group's other partials and merges them.
+//   * Attention partials are tagged words too. The items holding a (lane, KV head) group's
+//     last chunks wait for the group's other partials and merge them, a set of heads each.
 //   * Weights and the KV cache are streamed with non-temporal 128-bit buffer loads.
 #pragma once
 #include <hip/hip_runtime.h>

@@ -17,7 +17,7 @@ namespace fm {
 // One instruction: op (FM_OP_*), layer, and an operand range whose meaning depends on op:
 //   GEMV ops  -> output rows [a, b) of that op's matrix (QKV rows index [W_q; W_k; W_v]),
 //   FM_OP_ATTN -> attention work item a of the layer (mapped to lane/KV head/slots per step;
-//                 the item with a (lane, KV head) group's last chunk also merges its partials).
+//                 a (lane, KV head) group's last items also merge its partials, a head set each).
 struct Instr {
   int32_t op, layer, a, b;
 };
